@@ -1,0 +1,208 @@
+"""Benchmark of the DEX decode step on one MI355X.
+
+A step is one dex_step call: one round of Algorithm 1 (every stage that has
+lattice rows streams its layers once, then the batched exit head, verify /
+commit and the key/value collapse).  The value is committed tokens per
+second over the timed steps, inputs and weights already resident in HBM.
+
+Prints one JSON line.  Besides the contract fields it carries
+  roofline     for the dominant kernel: algorithmic bytes per launch over its
+               mean launch duration (HIP events on the decode stream, over a
+               second instrumented run of the same number of steps), against
+               the 8 TB/s HBM peak;
+  cpu_baseline the oracle (float64 numpy) running the same decode on the host
+               cores for a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from synth import configs, gen  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=128)
+    p.add_argument("--warmup", type=int, default=8)
+    p.add_argument("--config", default=configs.HEADLINE)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=20.0)
+    p.add_argument("--no-ar", action="store_true", help="skip the plain AR reference rate")
+    p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    return p.parse_args()
+
+
+def cpu_baseline(cfg, weights, prompts, budget_s):
+    """The oracle as it stands, timed on this host: DEX rounds on the first
+    sequence after its prefill (prefill untimed)."""
+    import oracle
+    from oracle import dex
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = None
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, weights))
+    prompt = [int(t) for t in prompts[0]]
+    pf = m.prefill(prompt)
+    # run DEX for growing T until the budget is used; report the last full run
+    T, t_used, commits, rounds = 2, 0.0, 0, 0
+    while True:
+        t0 = time.perf_counter()
+        r = dex.dex_generate(m, prompt, cfg["explored"], cfg["width_cap"], bool(cfg["decs"]), T,
+                             prefill=pf, keep_trace=False)
+        dt = time.perf_counter() - t0
+        t_used, commits, rounds = dt, T - 1, r.rounds
+        if dt * 2.5 > budget_s or T >= cfg["gen_len"]:
+            break
+        T = min(cfg["gen_len"], T * 2)
+    cores = len(os.sched_getaffinity(0))
+    return {
+        "value": commits / t_used, "unit": "committed tokens/s", "cores": blas_threads or cores,
+        "kind": "oracle",
+        "sample": f"float64 oracle DEX on sequence 0 of {cfg['name']}: {cfg['prompt_len']}-token prompt "
+                  f"(prefill untimed), {commits} commits in {rounds} rounds, {t_used:.1f} s; "
+                  f"host affinity {cores} cores",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2606_29223_amd import dexlib
+
+    cfg = configs.get(args.config)
+    t0 = time.time()
+    weights = gen.generate_model(cfg)
+    prompts = gen.prompts(cfg)
+    dev_w = dexlib.device_weights(cfg, weights)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    P = cfg["prompt_len"]
+    max_ctx = P + cfg["gen_len"]
+    need = args.warmup + 2 * args.steps + 2
+    if need > cfg["gen_len"]:
+        max_ctx = P + need
+
+    dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx)
+    dec.prefill(prompts)
+    B = dec.batch
+
+    def steps(n):
+        commits = rounds = layers = row_layers = 0
+        for _ in range(n):
+            c = dec.step()
+            commits += int((c >= 0).sum())
+            rounds += 1
+            layers += dec.info.layers_streamed
+            row_layers += dec.info.row_layers
+        return commits, rounds, layers, row_layers
+
+    steps(args.warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    commits, rounds, layers, row_layers = steps(args.steps)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    value = commits / elapsed
+
+    # instrumented run of the same length: per-kernel HIP event durations
+    dec.set_timing(True)
+    steps(args.steps)
+    torch.cuda.synchronize()
+    ms, n, nbytes = dec.kernel_times()
+    dec.set_timing(False)
+    dec.close()
+    names = dexlib.KERNEL_CLASSES
+    dom = max(range(7), key=lambda i: ms[i])
+    avg_ms = ms[dom] / max(1, n[dom])
+    bytes_per = nbytes[dom] / max(1, n[dom])
+    achieved = bytes_per / (avg_ms * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            tj = json.load(open(args.traffic_json))
+            ent = tj.get(cfg["name"], {}).get(names[dom])
+            if ent:
+                traffic = ent.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    roofline = {"bound": "hbm", "kernel": names[dom], "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "bytes_per_launch": bytes_per, "avg_launch_us": round(avg_ms * 1e3, 2),
+                "launches": int(n[dom])}
+    per_kernel = {names[i]: {"ms": round(ms[i], 3), "launches": int(n[i]),
+                             "GBps": round(nbytes[i] / max(ms[i], 1e-9) / 1e6, 1) if nbytes[i] else None}
+                  for i in range(8)}
+
+    ar_value = None
+    if not args.no_ar:
+        ar = dexlib.Decoder(cfg, dev_w, explored=[cfg["n_layers"]], width_cap=1, max_context=max_ctx)
+        ar.prefill(prompts)
+        for _ in range(args.warmup):
+            ar.step()
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        na = 0
+        for _ in range(args.steps):
+            na += int((ar.step() >= 0).sum())
+        torch.cuda.synchronize()
+        ar_value = na / (time.perf_counter() - ta)
+        ar.close()
+
+    L, N = cfg["n_layers"], len(cfg["explored"])
+    cpu = None
+    if not args.no_cpu_baseline:
+        del dev_w
+        torch.cuda.empty_cache()
+        cpu = cpu_baseline(cfg, weights, prompts, args.cpu_seconds)
+
+    out = {
+        "metric": "committed tokens/s at batch 1 (32L d4096 bf16) + achieved HBM GB/s vs peak",
+        "value": round(value, 3),
+        "unit": "committed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
+        "data": "synthetic (seeded random weights and uniform prompts)",
+        "config": {"workload": cfg["name"], "explored": cfg["explored"], "width_cap": cfg["width_cap"],
+                   "batch": B, "prompt_len": P, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "dex": {"commits": commits, "rounds": rounds, "rounds_per_commit": round(rounds / max(commits, 1), 4),
+                "weight_layers_streamed_per_commit": round(layers / max(commits, 1), 3),
+                "row_layers_per_commit": round(row_layers / max(commits, 1), 3),
+                "critical_path_layers_per_commit": round(L / N * rounds / max(commits, 1), 3),
+                "ar_layers_per_commit": L},
+        "ar_tokens_per_s": round(ar_value, 3) if ar_value else None,
+        "kernels": per_kernel,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

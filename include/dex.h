@@ -1,0 +1,203 @@
+/*
+ * dex.h -- C ABI of the MI355X (gfx950) Depth Exploration Decoding library.
+ *
+ * One library context decodes `batch` independent sequences, each with its
+ * own depth-position lattice, greedily, exactly as Algorithm 1 of the paper
+ * ("Depth Exploration for LLM Decoding") describes:
+ *   - dex_create    : a model with exit depths and an explored-depth set X
+ *                     (Definition 3: d_0 < ... < d_{N-1} = L) go in;
+ *                     stage k is the layer range (d_{k-1}, d_k] (Algorithm 1,
+ *                     Require clause).
+ *   - dex_prefill   : Algorithm 1's init -- the prompt's keys/values and the
+ *                     first generated token (final-depth argmax at the last
+ *                     prompt position).
+ *   - dex_step      : one iteration of Algorithm 1's loop (expand, DECS,
+ *                     insert, and when the anchor reaches the final depth
+ *                     validate-and-commit then collapse) for every sequence;
+ *                     commits at most one token per sequence.
+ *   - dex_destroy   : frees everything the library allocated.
+ *
+ * The committed tokens equal greedy autoregressive decoding of the same
+ * model (the lossless invariant of Section 3.2); with X = {L} and
+ * width_cap = 1 each dex_step is one plain autoregressive step.
+ *
+ * Conventions
+ *   - Every call returns dex_status; DEX_OK is 0, errors are negative.  No
+ *     C++ exception crosses the ABI.  dex_last_error(ctx) gives a message
+ *     (dex_last_error(NULL): the last dex_create failure of this thread).
+ *   - Weights are borrowed DEVICE memory: the caller keeps them alive and
+ *     unchanged until dex_destroy.  Every array is row-major; a projection
+ *     matrix is [out_features][in_features].  The library owns the key/value
+ *     caches, the lattice state and all scratch memory.
+ *   - Host arrays passed in or out are caller-owned and only accessed during
+ *     the call.
+ *   - All device work is enqueued on config.hip_stream (NULL = the default
+ *     stream).  dex_prefill and dex_step synchronise that stream before
+ *     returning host results.  A context is not thread-safe.
+ *   - After any failure inside dex_prefill or dex_step the context is
+ *     poisoned: later calls return DEX_E_STATE.
+ */
+#ifndef DEX_H
+#define DEX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dex_ctx dex_ctx;
+
+typedef enum {
+  DEX_OK = 0,
+  DEX_E_INVAL = -1,     /* bad argument (dims, explored set, sizes, null pointers) */
+  DEX_E_NOMEM = -2,     /* device or host allocation failed */
+  DEX_E_HIP = -3,       /* a HIP runtime call failed; message in dex_last_error */
+  DEX_E_STATE = -4,     /* call out of order (step before prefill) or poisoned context */
+  DEX_E_CAPACITY = -5   /* max_context or lattice capacity exhausted */
+} dex_status;
+
+typedef enum { DEX_F32 = 0, DEX_BF16 = 1 } dex_dtype;
+
+/* Per-layer parameter order inside dex_model.layers. */
+enum {
+  DEX_P_ATTN_NORM = 0,  /* float [d]                    RMSNorm gain before attention */
+  DEX_P_WQ = 1,         /* weight [H*hd][d]             query projection */
+  DEX_P_WK = 2,         /* weight [Hkv*hd][d]           key projection */
+  DEX_P_WV = 3,         /* weight [Hkv*hd][d]           value projection */
+  DEX_P_WO = 4,         /* weight [d][H*hd]             attention output projection */
+  DEX_P_FFN_NORM = 5,   /* float [d]                    RMSNorm gain before the FFN */
+  DEX_P_W_GATE = 6,     /* weight [F][d]                SwiGLU gate projection */
+  DEX_P_W_UP = 7,       /* weight [F][d]                SwiGLU up projection */
+  DEX_P_W_DOWN = 8,     /* weight [d][F]                SwiGLU down projection */
+  DEX_P_COUNT = 9
+};
+
+#define DEX_MAX_BATCH 64
+#define DEX_MAX_EXPLORED 32
+#define DEX_MAX_ROWS 256
+
+/* "A model with exit depths": a decoder-only Llama-family backbone whose
+ * shared final RMSNorm and LM head decode every explored depth (the paper's
+ * inducing-adapter appendix: intermediate depths use the same final
+ * normalisation and LM head).  Layer l (1-based) scales both residual
+ * branches by residual_scale * l / L.  RoPE is rotate-half with base
+ * rope_theta; attention scale 1/sqrt(head_dim); query head h reads key/value
+ * head h / (n_heads / n_kv_heads).  `weight_dtype` is the element type of the
+ * embedding, the projections and the LM head, and also of the key/value
+ * cache and the activations fed to the matrix cores; norm gains are float.
+ * Requirements: d_model, head_dim multiples of 16; head_dim <= 128;
+ * n_heads a multiple of n_kv_heads; n_heads/n_kv_heads <= 8.             */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  float rope_theta, rms_eps, residual_scale;
+  int32_t weight_dtype;                 /* dex_dtype */
+  const void *embed;                    /* device [vocab][d] */
+  const float *final_norm;              /* device [d] */
+  const void *lm_head;                  /* device [vocab][d] */
+  const void *const *layers;            /* HOST array [n_layers * DEX_P_COUNT] of device pointers */
+} dex_model;
+
+/* "An explored-depth set" plus execution limits. */
+typedef struct {
+  const int32_t *explored;              /* host [n_explored], strictly increasing in [1, L], last == L */
+  int32_t n_explored;                   /* N, 1 .. DEX_MAX_EXPLORED */
+  int32_t width_cap;                    /* lattice rows per round per sequence; 0 = uncapped
+                                           (the paper's binary lattice, needs 2^(N-1) rows) */
+  int32_t decs;                         /* 1: DECS masked argmax (Algorithm 2, greedy); 0: plain argmax */
+  int32_t batch;                        /* independent sequences, 1 .. DEX_MAX_BATCH */
+  int32_t max_context;                  /* prompt length + generated tokens, per sequence */
+  void *hip_stream;                     /* hipStream_t or NULL */
+} dex_config;
+
+/* What one dex_step did (all host memory).  Rows are listed stage-major,
+ * then by sequence, then in the lattice's priority order.                  */
+typedef struct {
+  int32_t n_rows;                       /* lattice nodes evaluated this round, all sequences */
+  int32_t rows_per_stage[DEX_MAX_EXPLORED];
+  int32_t layers_streamed;              /* layers of the stages that had >= 1 row */
+  int32_t row_layers;                   /* sum over rows of the layers each row ran */
+  int32_t q[DEX_MAX_BATCH];             /* FSM state (anchor's completed stages) at round start */
+  int32_t kstar[DEX_MAX_BATCH];         /* shallowest matching depth index if committed, else -1 */
+  int32_t row_seq[DEX_MAX_ROWS];
+  int32_t row_slot[DEX_MAX_ROWS];       /* canonical slot index within its sequence's lattice */
+  int32_t row_stage[DEX_MAX_ROWS];
+  int32_t row_pos[DEX_MAX_ROWS];        /* absolute position of the row's input token */
+  int32_t row_token[DEX_MAX_ROWS];      /* decoded candidate (DECS argmax) of the row */
+  int64_t rounds_total;                 /* dex_step calls so far */
+} dex_step_info;
+
+/* Validate the model and X, derive the stages, allocate caches and scratch.
+ * Errors: DEX_E_INVAL (dims, X not strictly increasing / not ending at L,
+ * rows per round above DEX_MAX_ROWS), DEX_E_NOMEM, DEX_E_HIP.              */
+dex_status dex_create(const dex_model *model, const dex_config *config, dex_ctx **out);
+
+/* Algorithm 1's init.  prompts: host [batch][prompt_len] token ids in
+ * [0, vocab).  Writes first_tokens[batch] (host): y_0 per sequence.  May be
+ * called again to restart decoding with new prompts.
+ * Errors: DEX_E_INVAL (ids, lengths), DEX_E_CAPACITY (prompt_len >= max_context). */
+dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t prompt_len, int32_t *first_tokens);
+
+/* One round for every sequence.  committed (host [batch]): the token a
+ * sequence committed this round, or -1.  info may be NULL.  A sequence whose
+ * committed length reached max_context takes no further part.
+ * Errors: DEX_E_STATE (no prefill yet / poisoned), DEX_E_CAPACITY (every
+ * sequence is full, or the lattice outgrew its slot capacity), DEX_E_HIP.   */
+dex_status dex_step(dex_ctx *ctx, int32_t *committed, dex_step_info *info);
+
+/* Frees every library-owned allocation.  NULL-safe. */
+void dex_destroy(dex_ctx *ctx);
+
+const char *dex_last_error(const dex_ctx *ctx);
+
+/* ---------------------------------------------------------------------------
+ * Inspection taps for tests and the benchmark.
+ * ------------------------------------------------------------------------- */
+
+/* While enabled, every dex_step writes the float32 exit logits (before the
+ * DECS mask) of each round row r to device_buf + r * vocab.  capacity_rows
+ * must be >= the rows a round can have.  device_buf NULL disables.          */
+dex_status dex_debug_set_logits_tap(dex_ctx *ctx, float *device_buf, int32_t capacity_rows);
+
+/* Slot table of sequence `seq` in canonical order, each slot written as
+ * stride = 5 + N int32: x, pos, parent (-1 for the anchor), fork stage, c,
+ * then u[0..N-1] (-1 where not computed).  *n_slots receives the count.     */
+dex_status dex_debug_lattice(dex_ctx *ctx, int32_t seq, int32_t *out, int32_t capacity_slots, int32_t *n_slots);
+
+/* The last collapse of sequence `seq`: old canonical indices of the retained
+ * slots (in order), whether the new anchor is fresh, and the committed
+ * position the old anchor's keys/values went to.                            */
+dex_status dex_debug_last_collapse(dex_ctx *ctx, int32_t seq, int32_t *map, int32_t capacity,
+                                   int32_t *n_map, int32_t *fresh, int32_t *committed_pos);
+
+/* Key/value cache layout: element (layer l, seq s, kv head g, entry e, dim i)
+ * is at base + (((l * batch + s) * n_kv_heads + g) * entries + e) * head_dim + i
+ * with entries returned in *entries.  Entry p < max_context is committed
+ * position p; lattice slot j of seq s lives at entry lattice_entry(s, j)
+ * (see dex_debug_slot_entry).                                                */
+dex_status dex_debug_kv_layout(dex_ctx *ctx, void **k_base, void **v_base, int64_t *entries);
+dex_status dex_debug_slot_entry(dex_ctx *ctx, int32_t seq, int32_t slot, int32_t *entry);
+
+/* Kernel timing: while enabled, hipEvents bracket every launch of the layer
+ * kernels on the context's stream.  dex_debug_kernel_times fills, for each
+ * kernel class c < n (0 qkv, 1 attention, 2 attention combine, 3 o-proj,
+ * 4 gate/up, 5 down, 6 lm-head, 7 other), the summed milliseconds and the
+ * launch count since the last reset, and the algorithmic bytes moved by those
+ * launches (weights + activations + keys/values they read or write).          */
+dex_status dex_debug_set_kernel_timing(dex_ctx *ctx, int32_t enable);
+dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *launches, double *bytes);
+
+/* Stand-alone skinny GEMM y[M][N] = x[M][K] * W[N][K]^T (float32 out) on the
+ * same matrix-core kernel the decode step uses.  dtype: dex_dtype of W and x.
+ * Device pointers; M in [1, 64].  For tests of batch invariance.            */
+dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M,
+                          float *y, void *hip_stream);
+
+/* Plain device copy of `bytes` (multiple of 16) used to calibrate hardware
+ * traffic counters against a kernel of known size.                          */
+dex_status dex_debug_copy(void *dst, const void *src, int64_t bytes, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DEX_H */

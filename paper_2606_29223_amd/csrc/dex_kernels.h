@@ -1,0 +1,145 @@
+// Internal declarations shared by the HIP kernels and the host engine.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dex {
+
+typedef uint16_t bf16;
+
+// ---------------------------------------------------------------- epilogues
+enum Epi {
+  EPI_PLAIN = 0,   // y[m][n] (float)
+  EPI_QKV = 1,     // rms-scaled, RoPE on q/k, q -> float buffer, k/v -> cache
+  EPI_RESID = 2,   // h += alpha * y; next-norm input and sum-of-squares partials
+  EPI_SWIGLU = 3,  // rms-scaled gate/up pair -> SiLU(gate) * up
+  EPI_LOGITS = 4,  // rms-scaled LM head, DECS mask, per-tile argmax
+};
+
+constexpr int GEMM_WAVES = 8;       // split-K ways inside a workgroup
+constexpr int GEMM_THREADS = GEMM_WAVES * 64;
+constexpr int ATT_SPLIT = 256;      // logical keys per attention split
+constexpr int ATT_TILE = 64;        // keys per LDS tile
+constexpr int ATT_THREADS = 256;
+constexpr int ATT_MAX_PAIRS = 64;   // (row, query head) pairs per attention workgroup
+
+struct GemmArgs {
+  // Weight segments concatenated along the output dimension (QKV uses three,
+  // SWIGLU uses w0 = gate and w1 = up paired column for column).
+  const void *w0, *w1, *w2;
+  int n0, n1, n2;
+  int N;          // output columns (SWIGLU: d_ffn)
+  int K;
+  const void *x;  // activations [M][ldx]
+  int ldx;
+  int M;
+  // RMSNorm scale from sum-of-squares partials (nullable): per row
+  // 1/sqrt(sum(part[m][0..n_part)) * inv_d + eps).
+  const float *part;
+  int n_part;
+  float inv_d, eps;
+  // PLAIN / QKV: float output [M][ld_out]
+  float *out;
+  int ld_out;
+  // QKV
+  void *kc, *vc;              // this layer's cache base ([B][Hkv][E][hd])
+  int kv_entries;             // E
+  int n_heads, n_kv_heads, head_dim;
+  const int *row_seq, *row_pos, *row_entry;
+  const float2 *rope;         // [max_ctx][hd/2] (cos, sin)
+  // RESID
+  float *h;                   // [M][ld_h] residual stream (in place)
+  int ld_h;
+  float alpha;
+  const float *g_next;        // gain of the next RMSNorm (nullable)
+  void *xb;                   // next-norm input g*h (T) [M][ld_h] (nullable)
+  float *part_out;            // [M][n_part_out]
+  int n_part_out;
+  const int *row_bnd;         // nullable: write h/partials to boundary storage instead
+  float *bnd_h, *bnd_part;
+  // SWIGLU
+  void *act;                  // [M][ld_act] (T)
+  int ld_act;
+  // LOGITS
+  const int *mask_tok;        // [M][mask_stride]
+  const int *mask_n;          // [M]
+  int mask_stride;
+  float *logits_tap;          // nullable [M][N]
+  float2 *amax;               // [M][n_tiles] (value, index as float bits)
+  int n_tiles;
+};
+
+struct AttnArgs {
+  const float *q;             // [R][H*hd], RoPE applied
+  int ldq;
+  const void *kc, *vc;        // this layer's cache base
+  int kv_entries, n_kv_heads, n_heads, head_dim, batch;
+  // row groups: consecutive rows of one sequence
+  const int *grp_row0, *grp_nrows, *grp_seq;
+  const int *row_pos, *row_nc, *row_chain_off, *chain;
+  float *part;                // [R][H][jmax][hd + 2]
+  int jmax;
+  float scale;
+};
+
+struct CombineArgs {
+  const float *part;
+  const int *row_pos;
+  int jmax, n_heads, head_dim;
+  void *out;                  // [R][H*hd] (T)
+  int ld_out;
+};
+
+// Launchers (return the HIP status of the launch).
+hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipStream_t s);
+hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s);
+hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s);
+
+struct PrepArgs {
+  int M, d, n_part;
+  int from_embed;             // 1: h = E[token]; 0: h = boundary[src]
+  const int *row_tok;         // embed token per row
+  const int *row_src;         // boundary index per row
+  const void *embed;
+  const float *bnd_h, *bnd_part;
+  const float *g;             // gain of the first RMSNorm the rows meet
+  float *h, *part;            // [M][d], [M][n_part]
+  void *xb;                   // [M][d] (T)
+  const int *row_out;         // nullable: write h/part to row_out[m] instead of m
+};
+hipError_t launch_prep(int dtype, const PrepArgs &a, hipStream_t s);
+
+struct ArgmaxArgs {
+  const float2 *amax;
+  int n_tiles, M;
+  int *u_out;                 // [M]
+  int *cand;                  // [..][N] candidate table (nullable)
+  const int *row_cand;        // [M] index into cand (slot*N + stage)
+};
+hipError_t launch_argmax(const ArgmaxArgs &a, hipStream_t s);
+
+struct CommitArgs {
+  int n;                      // sequences committing this round
+  const int *seq_cand;        // [n] candidate table offset of the anchor (slot*N)
+  int N;
+  const int *cand;
+  int *out;                   // [n][2] (token, kstar)
+};
+hipError_t launch_commit(const CommitArgs &a, hipStream_t s);
+
+struct CollapseArgs {
+  int n_jobs;
+  const int *job;             // [n_jobs][4]: seq, src entry/slot, dst entry/slot, kind (0 kv only, 1 kv + slot state)
+  void *kc, *vc;              // cache base
+  int n_layers, batch, n_kv_heads, kv_entries, head_dim;
+  int elem_bytes;
+  float *bnd_h, *bnd_part;    // [B][2S][d], [B][2S][n_part]
+  int *cand;                  // [B][2S][N]
+  int slots2, d, n_part, N, max_ctx, S;
+};
+hipError_t launch_collapse(const CollapseArgs &a, hipStream_t s);
+
+hipError_t launch_copy(void *dst, const void *src, int64_t bytes, hipStream_t s);
+
+}  // namespace dex

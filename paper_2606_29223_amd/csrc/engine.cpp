@@ -1,0 +1,1047 @@
+// Host engine of the DEX library: lattice planner (Algorithm 1's expand /
+// insert / validate-and-commit / collapse / advance, Section 3.2), the
+// key/value and lattice-slot memory manager, the round executor that drives
+// the gfx950 kernels, prefill, and the C ABI declared in include/dex.h.
+//
+// Device memory layout (all owned by the context):
+//   K/V cache     T [L][B][Hkv][E][hd]; entry e < max_context is committed
+//                 position e; entries max_context + p*S + i hold lattice slot
+//                 i of half p (the two halves alternate at every collapse).
+//   slot state    float h [B][2S][d] and sum-of-squares partials
+//                 [B][2S][d/16] of each slot's last completed stage, and its
+//                 candidate tokens int [B][2S][N].
+//   round scratch rows x {h, partials, norm input, q, attention out, SwiGLU
+//                 out}, attention split partials, LM-head tile winners.
+// One host->device copy of the round's row tables, one device->host copy of
+// the decoded candidates and commits per round.
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "dex.h"
+#include "dex_kernels.h"
+
+using namespace dex;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+struct Slot {
+  int x = 0, pos = 0, parent = -1, fork_stage = -1, c = 0;
+  std::vector<int> u;        // candidates of completed stages
+  std::vector<int> child;    // child slot per fork stage, -1 if none
+};
+
+struct Seq {
+  std::vector<int> committed;   // prompt + generated tokens
+  std::vector<Slot> slots;      // canonical order, slots[0] = anchor
+  int half = 0;                 // lattice half holding the slots
+  bool active = false;
+  std::vector<int> last_map;
+  int last_fresh = -1, last_committed_pos = -1;
+};
+
+struct Item {
+  int kind;                 // 0 advance, 1 fork
+  int slot, f;
+  std::vector<int> path;
+  int cost;
+};
+
+struct Timing {
+  int cls;
+  hipEvent_t a, b;
+  double bytes;
+};
+
+inline bool item_less(const Item &a, const Item &b) {
+  if (a.cost != b.cost) return a.cost < b.cost;
+  if (a.path.size() != b.path.size()) return a.path.size() < b.path.size();
+  return a.path < b.path;
+}
+
+}  // namespace
+
+struct dex_ctx {
+  // model
+  int L, d, H, Hkv, hd, F, V, dtype, es;
+  float theta, eps, rscale;
+  const void *embed, *lm_head;
+  const float *final_norm;
+  std::vector<const void *> lw;   // [L][9]
+  // config
+  std::vector<int> X;
+  int N, W, decs, B, max_ctx;
+  hipStream_t stream;
+  std::vector<std::vector<int>> stage_layers;
+  // capacities
+  int S, R_max, CH_MAX, E, n_part, jmax;
+  // device buffers
+  void *kc = nullptr, *vc = nullptr;
+  float2 *rope = nullptr;
+  float *bnd_h = nullptr, *bnd_part = nullptr;
+  int *cand = nullptr;
+  float *h_w = nullptr, *part_w = nullptr, *q_w = nullptr, *attn_part = nullptr;
+  void *xb_w = nullptr, *att_w = nullptr, *act_w = nullptr;
+  float *ex_h = nullptr, *ex_part = nullptr;
+  void *ex_xb = nullptr;
+  float2 *amax = nullptr;
+  int *u_dev = nullptr, *commit_dev = nullptr;
+  int *tab_dev = nullptr;
+  size_t tab_cap = 0;
+  int *job_dev = nullptr;
+  // pinned host staging
+  int *tab_host = nullptr, *res_host = nullptr, *job_host = nullptr;
+  // state
+  std::vector<Seq> seqs;
+  bool prefilled = false, poisoned = false;
+  int64_t rounds = 0;
+  std::string err;
+  float *logits_tap = nullptr;
+  int logits_cap = 0;
+  // timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_next = 0;
+  std::vector<Timing> pending;
+  double t_ms[8] = {0}, t_bytes[8] = {0};
+  int64_t t_n[8] = {0};
+  std::vector<void *> allocs;
+};
+
+namespace {
+
+#define HIPCHK(expr)                                                          \
+  do {                                                                        \
+    hipError_t e_ = (expr);                                                   \
+    if (e_ != hipSuccess) {                                                   \
+      ctx->err = std::string(#expr) + ": " + hipGetErrorString(e_);           \
+      return DEX_E_HIP;                                                       \
+    }                                                                         \
+  } while (0)
+
+dex_status dalloc(dex_ctx *ctx, void **p, size_t bytes) {
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    ctx->err = "hipMalloc of " + std::to_string(bytes) + " bytes failed: " + hipGetErrorString(e);
+    *p = nullptr;
+    return DEX_E_NOMEM;
+  }
+  ctx->allocs.push_back(*p);
+  return DEX_OK;
+}
+
+void dfree(dex_ctx *ctx, void *p) {
+  if (!p) return;
+  auto it = std::find(ctx->allocs.begin(), ctx->allocs.end(), p);
+  if (it != ctx->allocs.end()) ctx->allocs.erase(it);
+  (void)hipFree(p);
+}
+
+const void *LW(const dex_ctx *ctx, int l, int p) { return ctx->lw[(size_t)l * DEX_P_COUNT + p]; }
+
+// --------------------------------------------------------------- timing
+hipEvent_t next_event(dex_ctx *ctx) {
+  if (ctx->ev_next >= ctx->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    ctx->ev_pool.push_back(e);
+  }
+  return ctx->ev_pool[ctx->ev_next++];
+}
+
+struct TimedLaunch {
+  dex_ctx *ctx;
+  int cls;
+  double bytes;
+  hipEvent_t a = nullptr;
+  TimedLaunch(dex_ctx *c, int cl, double b) : ctx(c), cls(cl), bytes(b) {
+    if (ctx->timing) {
+      a = next_event(ctx);
+      if (a) (void)hipEventRecord(a, ctx->stream);
+    }
+  }
+  ~TimedLaunch() {
+    if (ctx->timing && a) {
+      hipEvent_t b = next_event(ctx);
+      if (b) {
+        (void)hipEventRecord(b, ctx->stream);
+        ctx->pending.push_back({cls, a, b, bytes});
+      }
+    }
+  }
+};
+
+void harvest_timing(dex_ctx *ctx) {
+  for (auto &t : ctx->pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
+      ctx->t_ms[t.cls] += ms;
+      ctx->t_n[t.cls] += 1;
+      ctx->t_bytes[t.cls] += t.bytes;
+    }
+  }
+  ctx->pending.clear();
+  ctx->ev_next = 0;
+}
+
+// ---------------------------------------------------------- lattice rules
+std::vector<int> slot_path(const Seq &s, int i) {
+  std::vector<int> p;
+  while (s.slots[i].parent >= 0) {
+    p.push_back(s.slots[i].fork_stage);
+    i = s.slots[i].parent;
+  }
+  std::reverse(p.begin(), p.end());
+  return p;
+}
+
+std::vector<int> ancestors(const Seq &s, int i) {   // anchor first, parent last
+  std::vector<int> a;
+  int p = s.slots[i].parent;
+  while (p >= 0) {
+    a.push_back(p);
+    p = s.slots[p].parent;
+  }
+  std::reverse(a.begin(), a.end());
+  return a;
+}
+
+// Work items of one round in priority order (anchor first).  Same rule as
+// the lattice definition: advance a non-anchor slot only when every ancestor
+// completed more stages at round start; fork every completed stage f <= N-2
+// not yet forked (without DECS, not when its token repeats a shallower fork
+// of the same slot); width cap keeps the anchor and the W-1 items of lowest
+// (hypothesis cost, path length, path).
+std::vector<Item> plan_items(const dex_ctx *ctx, const Seq &s) {
+  std::vector<Item> items;
+  const int N = ctx->N;
+  for (int i = 0; i < (int)s.slots.size(); ++i) {
+    const Slot &sl = s.slots[i];
+    const std::vector<int> path = slot_path(s, i);
+    int cost = 0;
+    for (int f : path) cost += f + 1;
+    bool adv = (i == 0);
+    if (!adv) {
+      adv = true;
+      for (int a : ancestors(s, i))
+        if (s.slots[a].c <= sl.c) { adv = false; break; }
+    }
+    if (adv) items.push_back({0, i, -1, path, cost});
+    if (sl.pos + 1 > ctx->max_ctx - 1) continue;
+    for (int f = 0; f < std::min(sl.c, N - 1); ++f) {
+      if (sl.child[f] >= 0) continue;
+      if (!ctx->decs) {
+        bool dup = false;
+        for (int g = 0; g < f; ++g) dup |= (sl.u[g] == sl.u[f]);
+        if (dup) continue;
+      }
+      std::vector<int> p2 = path;
+      p2.push_back(f);
+      items.push_back({1, i, f, p2, cost + f + 1});
+    }
+  }
+  std::vector<Item> rest(items.begin() + 1, items.end());
+  std::sort(rest.begin(), rest.end(), item_less);
+  if (ctx->W > 0 && (int)rest.size() > ctx->W - 1) rest.resize(ctx->W - 1);
+  std::vector<Item> out;
+  out.push_back(items[0]);
+  out.insert(out.end(), rest.begin(), rest.end());
+  return out;
+}
+
+struct Row {
+  int seq, slot, stage;
+};
+
+inline int slot_entry(const dex_ctx *ctx, const Seq &s, int slot) { return ctx->max_ctx + s.half * ctx->S + slot; }
+inline int slot_global(const dex_ctx *ctx, int seq, const Seq &s, int slot) {
+  return seq * 2 * ctx->S + s.half * ctx->S + slot;
+}
+
+// ------------------------------------------------------- kernel drivers
+struct StageTables {
+  const int *seq, *pos, *entry, *bnd, *tok, *nc, *chain_off, *chain, *mask_n, *mask_tok, *cand_idx;
+  const int *g_row0, *g_nrows, *g_seq;
+  int n_groups;
+};
+
+double wbytes(const dex_ctx *ctx, double elems) { return elems * ctx->es; }
+
+dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, const StageTables &t,
+                      float *h, float *part, void *xb, float *q, void *att, void *act, float *apart,
+                      int jmax, bool to_boundary, const int *bnd_rows) {
+  const hipStream_t st = ctx->stream;
+  const int d = ctx->d, H = ctx->H, Hkv = ctx->Hkv, hd = ctx->hd, F = ctx->F;
+  const size_t layer_kv = (size_t)ctx->B * Hkv * ctx->E * hd * ctx->es;
+  for (int l = first_layer; l <= last_layer; ++l) {
+    const float alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
+    // QKV
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_WQ); a.w1 = LW(ctx, l, DEX_P_WK); a.w2 = LW(ctx, l, DEX_P_WV);
+      a.n0 = H * hd; a.n1 = Hkv * hd; a.n2 = Hkv * hd;
+      a.N = (H + 2 * Hkv) * hd; a.K = d;
+      a.x = xb; a.ldx = d; a.M = M;
+      a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+      a.out = q; a.ld_out = H * hd;
+      a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
+      a.kv_entries = ctx->E; a.n_heads = H; a.n_kv_heads = Hkv; a.head_dim = hd;
+      a.row_seq = t.seq; a.row_pos = t.pos; a.row_entry = t.entry; a.rope = ctx->rope;
+      TimedLaunch tl(ctx, 0, wbytes(ctx, (double)a.N * d + (double)M * d + 2.0 * M * Hkv * hd) + 4.0 * M * H * hd);
+      HIPCHK(launch_gemm(ctx->dtype, EPI_QKV, a, 1, st));
+    }
+    // attention + combine
+    {
+      AttnArgs a{};
+      a.q = q; a.ldq = H * hd;
+      a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
+      a.kv_entries = ctx->E; a.n_kv_heads = Hkv; a.n_heads = H; a.head_dim = hd; a.batch = ctx->B;
+      a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq;
+      a.row_pos = t.pos; a.row_nc = t.nc; a.row_chain_off = t.chain_off; a.chain = t.chain;
+      a.part = apart; a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
+      TimedLaunch tl(ctx, 1, 0.0);
+      HIPCHK(launch_attention(ctx->dtype, a, t.n_groups, st));
+    }
+    {
+      CombineArgs c{};
+      c.part = apart; c.row_pos = t.pos; c.jmax = jmax; c.n_heads = H; c.head_dim = hd;
+      c.out = att; c.ld_out = H * hd;
+      TimedLaunch tl(ctx, 2, 0.0);
+      HIPCHK(launch_combine(ctx->dtype, c, M, st));
+    }
+    // O projection + residual
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_WO); a.n0 = d; a.N = d; a.K = H * hd;
+      a.x = att; a.ldx = H * hd; a.M = M;
+      a.h = h; a.ld_h = d; a.alpha = alpha;
+      a.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM); a.xb = xb;
+      a.part_out = part; a.n_part_out = ctx->n_part;
+      TimedLaunch tl(ctx, 3, wbytes(ctx, (double)d * H * hd + (double)M * H * hd + (double)M * d) + 8.0 * M * d);
+      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, st));
+    }
+    // gate/up + SiLU
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_W_GATE); a.w1 = LW(ctx, l, DEX_P_W_UP);
+      a.n0 = F; a.N = F; a.K = d;
+      a.x = xb; a.ldx = d; a.M = M;
+      a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+      a.act = act; a.ld_act = F;
+      TimedLaunch tl(ctx, 4, wbytes(ctx, 2.0 * F * d + (double)M * d + (double)M * F));
+      HIPCHK(launch_gemm(ctx->dtype, EPI_SWIGLU, a, 1, st));
+    }
+    // down + residual
+    {
+      const bool last = (l == last_layer);
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_W_DOWN); a.n0 = d; a.N = d; a.K = F;
+      a.x = act; a.ldx = F; a.M = M;
+      a.h = h; a.ld_h = d; a.alpha = alpha;
+      a.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
+      a.xb = last ? nullptr : xb;
+      a.part_out = part; a.n_part_out = ctx->n_part;
+      if (last && to_boundary) {
+        a.row_bnd = bnd_rows; a.bnd_h = ctx->bnd_h; a.bnd_part = ctx->bnd_part;
+      }
+      TimedLaunch tl(ctx, 5, wbytes(ctx, (double)d * F + (double)M * F + (double)M * d) + 8.0 * M * d);
+      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, st));
+    }
+  }
+  return DEX_OK;
+}
+
+// exit head over M rows whose final state sits in (src_h, src_part)[row_src[m]]
+dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h, const float *src_part,
+                    const int *mask_n, const int *mask_tok, const int *cand_idx, int *cand) {
+  const hipStream_t st = ctx->stream;
+  {
+    PrepArgs p{};
+    p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = 0;
+    p.row_src = row_src; p.bnd_h = src_h; p.bnd_part = src_part; p.g = ctx->final_norm;
+    p.h = ctx->ex_h; p.part = ctx->ex_part; p.xb = ctx->ex_xb;
+    TimedLaunch tl(ctx, 7, 0.0);
+    HIPCHK(launch_prep(ctx->dtype, p, st));
+  }
+  const int n_tiles = (ctx->V + 15) / 16;
+  {
+    GemmArgs a{};
+    a.w0 = ctx->lm_head; a.n0 = ctx->V; a.N = ctx->V; a.K = ctx->d;
+    a.x = ctx->ex_xb; a.ldx = ctx->d; a.M = M;
+    a.part = ctx->ex_part; a.n_part = ctx->n_part; a.inv_d = 1.0f / ctx->d; a.eps = ctx->eps;
+    a.mask_n = mask_n; a.mask_tok = mask_tok; a.mask_stride = ctx->N;
+    a.logits_tap = ctx->logits_tap; a.amax = ctx->amax; a.n_tiles = n_tiles;
+    TimedLaunch tl(ctx, 6, wbytes(ctx, (double)ctx->V * ctx->d + (double)M * ctx->d));
+    HIPCHK(launch_gemm(ctx->dtype, EPI_LOGITS, a, 1, st));
+  }
+  {
+    ArgmaxArgs g{};
+    g.amax = ctx->amax; g.n_tiles = n_tiles; g.M = M; g.u_out = ctx->u_dev;
+    g.cand = cand; g.row_cand = cand_idx;
+    TimedLaunch tl(ctx, 7, 0.0);
+    HIPCHK(launch_argmax(g, st));
+  }
+  return DEX_OK;
+}
+
+dex_status fail(dex_ctx *ctx, dex_status s) {
+  if (s != DEX_OK && s != DEX_E_INVAL && s != DEX_E_CAPACITY) ctx->poisoned = true;
+  return s;
+}
+
+}  // namespace
+
+// ===================================================================== ABI
+extern "C" {
+
+const char *dex_last_error(const dex_ctx *ctx) {
+  if (ctx == nullptr) return g_create_error.c_str();
+  return ctx->err.c_str();
+}
+
+void dex_destroy(dex_ctx *ctx) {
+  if (!ctx) return;
+  if (ctx->stream) (void)hipStreamSynchronize(ctx->stream);
+  else (void)hipDeviceSynchronize();
+  for (void *p : ctx->allocs) (void)hipFree(p);
+  if (ctx->tab_host) (void)hipHostFree(ctx->tab_host);
+  if (ctx->res_host) (void)hipHostFree(ctx->res_host);
+  if (ctx->job_host) (void)hipHostFree(ctx->job_host);
+  for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
+  g_create_error.clear();
+  if (!out) { g_create_error = "out is NULL"; return DEX_E_INVAL; }
+  *out = nullptr;
+  if (!m || !c) { g_create_error = "model or config is NULL"; return DEX_E_INVAL; }
+  auto bad = [](const std::string &s) { g_create_error = s; return DEX_E_INVAL; };
+  if (m->n_layers < 1 || m->d_model < 16 || m->d_model % 16 || m->n_heads < 1 || m->n_kv_heads < 1 ||
+      m->n_heads % m->n_kv_heads || m->head_dim < 16 || m->head_dim % 16 || m->head_dim > 128 ||
+      m->d_ffn < 1 || m->vocab < 2)
+    return bad("model dimensions out of range");
+  if (m->n_heads / m->n_kv_heads > 8) return bad("n_heads / n_kv_heads must be <= 8");
+  if (m->weight_dtype != DEX_F32 && m->weight_dtype != DEX_BF16) return bad("weight_dtype must be DEX_F32 or DEX_BF16");
+  const int epb = m->weight_dtype == DEX_BF16 ? 8 : 4;
+  if (m->d_ffn % epb || (m->n_heads * m->head_dim) % epb) return bad("d_ffn must be a multiple of 8 (bf16) / 4 (f32)");
+  if (!m->embed || !m->final_norm || !m->lm_head || !m->layers) return bad("null weight pointer");
+  for (int i = 0; i < m->n_layers * DEX_P_COUNT; ++i)
+    if (!m->layers[i]) return bad("null layer weight pointer");
+  if (!(m->rms_eps >= 0.f) || !(m->rope_theta > 0.f)) return bad("rms_eps / rope_theta out of range");
+  if (c->n_explored < 1 || c->n_explored > DEX_MAX_EXPLORED || !c->explored) return bad("n_explored out of range");
+  for (int i = 0; i < c->n_explored; ++i) {
+    const int dd = c->explored[i];
+    if (dd < 1 || dd > m->n_layers || (i > 0 && dd <= c->explored[i - 1]))
+      return bad("explored depths must be strictly increasing in [1, L]");
+  }
+  if (c->explored[c->n_explored - 1] != m->n_layers) return bad("the last explored depth must be L");
+  if (c->batch < 1 || c->batch > DEX_MAX_BATCH) return bad("batch out of range");
+  if (c->width_cap < 0) return bad("width_cap must be >= 0");
+  if (c->max_context < 2) return bad("max_context must be >= 2");
+  const int N = c->n_explored;
+  long long per_seq = c->width_cap > 0 ? c->width_cap : (N - 1 >= 20 ? (1LL << 20) : (1LL << (N - 1)));
+  if (per_seq * c->batch > DEX_MAX_ROWS) return bad("rows per round exceed DEX_MAX_ROWS (lower width_cap or batch)");
+
+  dex_ctx *ctx = new dex_ctx();
+  ctx->L = m->n_layers; ctx->d = m->d_model; ctx->H = m->n_heads; ctx->Hkv = m->n_kv_heads;
+  ctx->hd = m->head_dim; ctx->F = m->d_ffn; ctx->V = m->vocab; ctx->dtype = m->weight_dtype;
+  ctx->es = ctx->dtype == DEX_BF16 ? 2 : 4;
+  ctx->theta = m->rope_theta; ctx->eps = m->rms_eps; ctx->rscale = m->residual_scale;
+  ctx->embed = m->embed; ctx->lm_head = m->lm_head; ctx->final_norm = m->final_norm;
+  ctx->lw.assign(m->layers, m->layers + (size_t)m->n_layers * DEX_P_COUNT);
+  ctx->X.assign(c->explored, c->explored + N);
+  ctx->N = N; ctx->W = c->width_cap; ctx->decs = c->decs ? 1 : 0; ctx->B = c->batch;
+  ctx->max_ctx = c->max_context; ctx->stream = (hipStream_t)c->hip_stream;
+  int prev = 0;
+  for (int k = 0; k < N; ++k) {
+    std::vector<int> ls;
+    for (int l = prev; l < ctx->X[k]; ++l) ls.push_back(l);
+    ctx->stage_layers.push_back(ls);
+    prev = ctx->X[k];
+  }
+  ctx->R_max = (int)per_seq * ctx->B;
+  ctx->S = ctx->W > 0 ? N * ctx->W + 1 : (int)per_seq;
+  ctx->CH_MAX = N + 1;
+  ctx->E = ctx->max_ctx + 2 * ctx->S;
+  ctx->n_part = ctx->d / 16;
+  ctx->jmax = (ctx->max_ctx + ATT_SPLIT - 1) / ATT_SPLIT;
+
+  dex_status st = DEX_OK;
+  auto A = [&](void **p, size_t bytes) {
+    if (st == DEX_OK) st = dalloc(ctx, p, bytes);
+  };
+  const size_t R = ctx->R_max, d = ctx->d, es = ctx->es;
+  const size_t kv_bytes = (size_t)ctx->L * ctx->B * ctx->Hkv * ctx->E * ctx->hd * es;
+  A(&ctx->kc, kv_bytes);
+  A(&ctx->vc, kv_bytes);
+  A((void **)&ctx->rope, (size_t)ctx->max_ctx * (ctx->hd / 2) * sizeof(float2));
+  const size_t slots_total = (size_t)ctx->B * 2 * ctx->S;
+  A((void **)&ctx->bnd_h, slots_total * d * 4);
+  A((void **)&ctx->bnd_part, slots_total * ctx->n_part * 4);
+  A((void **)&ctx->cand, slots_total * N * 4);
+  A((void **)&ctx->h_w, R * d * 4);
+  A((void **)&ctx->part_w, R * ctx->n_part * 4);
+  A(&ctx->xb_w, R * d * es);
+  A((void **)&ctx->q_w, R * ctx->H * ctx->hd * 4);
+  A(&ctx->att_w, R * ctx->H * ctx->hd * es);
+  A(&ctx->act_w, R * ctx->F * es);
+  A((void **)&ctx->attn_part, R * ctx->H * ctx->jmax * (ctx->hd + 2) * 4);
+  A((void **)&ctx->ex_h, R * d * 4);
+  A((void **)&ctx->ex_part, R * ctx->n_part * 4);
+  A(&ctx->ex_xb, R * d * es);
+  A((void **)&ctx->amax, R * ((ctx->V + 15) / 16) * sizeof(float2));
+  A((void **)&ctx->u_dev, R * 4 + 256);
+  A((void **)&ctx->commit_dev, (size_t)ctx->B * 2 * 4 + 256);
+  A((void **)&ctx->job_dev, (size_t)(ctx->B * (ctx->S + 1)) * 6 * 4 + 256);
+  ctx->tab_cap = (size_t)R * (16 + 2 * N + ctx->CH_MAX) + 4 * ctx->B + 1024;
+  A((void **)&ctx->tab_dev, ctx->tab_cap * 4);
+  if (st != DEX_OK) {
+    g_create_error = ctx->err;
+    dex_destroy(ctx);
+    return st;
+  }
+  if (hipHostMalloc((void **)&ctx->tab_host, ctx->tab_cap * 4) != hipSuccess ||
+      hipHostMalloc((void **)&ctx->res_host, (R + 2 * ctx->B + 64) * 4) != hipSuccess ||
+      hipHostMalloc((void **)&ctx->job_host, (size_t)(ctx->B * (ctx->S + 1)) * 6 * 4 + 256) != hipSuccess) {
+    g_create_error = "hipHostMalloc failed";
+    dex_destroy(ctx);
+    return DEX_E_NOMEM;
+  }
+  // RoPE table in double precision, rounded once: (cos, sin)(p * theta^(-2i/hd))
+  {
+    std::vector<float2> tab((size_t)ctx->max_ctx * (ctx->hd / 2));
+    for (int p = 0; p < ctx->max_ctx; ++p)
+      for (int i = 0; i < ctx->hd / 2; ++i) {
+        const double ang = (double)p * std::pow((double)ctx->theta, -2.0 * i / (double)ctx->hd);
+        tab[(size_t)p * (ctx->hd / 2) + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+      }
+    hipError_t e = hipMemcpy(ctx->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(ctx->kc, 0, kv_bytes);
+    if (e == hipSuccess) e = hipMemset(ctx->vc, 0, kv_bytes);
+    if (e == hipSuccess) e = hipMemset(ctx->cand, 0xff, slots_total * N * 4);
+    if (e != hipSuccess) {
+      g_create_error = std::string("initialisation copy failed: ") + hipGetErrorString(e);
+      dex_destroy(ctx);
+      return DEX_E_HIP;
+    }
+  }
+  ctx->seqs.resize(ctx->B);
+  *out = ctx;
+  return DEX_OK;
+}
+
+dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t *first) {
+  if (!ctx) return DEX_E_INVAL;
+  if (ctx->poisoned) { ctx->err = "context poisoned by an earlier failure"; return DEX_E_STATE; }
+  if (!prompts || !first || P < 1) { ctx->err = "bad prefill arguments"; return DEX_E_INVAL; }
+  if (P >= ctx->max_ctx) { ctx->err = "prompt_len must be < max_context"; return DEX_E_CAPACITY; }
+  const int B = ctx->B, d = ctx->d, H = ctx->H, hd = ctx->hd;
+  for (int i = 0; i < B * P; ++i)
+    if (prompts[i] < 0 || prompts[i] >= ctx->V) { ctx->err = "prompt token out of range"; return DEX_E_INVAL; }
+  const size_t M = (size_t)B * P, es = ctx->es;
+  const int G = H / ctx->Hkv;
+  const int grp_rows = std::max(1, ATT_MAX_PAIRS / G);
+  const int jmax = (P + ATT_SPLIT - 1) / ATT_SPLIT;
+  // attention row chunk bounded so its split partials stay below ~512 MiB
+  const size_t per_row = (size_t)H * jmax * (hd + 2) * 4;
+  size_t chunk = std::max<size_t>(grp_rows, (512ull << 20) / per_row);
+  chunk = std::min(chunk, M);
+  chunk = (chunk / grp_rows) * grp_rows;
+  if (chunk == 0) chunk = grp_rows;
+
+  float *h = nullptr, *part = nullptr, *q = nullptr, *apart = nullptr;
+  void *xb = nullptr, *att = nullptr, *act = nullptr;
+  int *tab = nullptr;
+  dex_status st = DEX_OK;
+  auto A = [&](void **p, size_t bytes) {
+    if (st == DEX_OK) st = dalloc(ctx, p, bytes);
+  };
+  A((void **)&h, M * d * 4);
+  A((void **)&part, M * ctx->n_part * 4);
+  A(&xb, M * d * es);
+  A((void **)&q, M * H * hd * 4);
+  A(&att, M * H * hd * es);
+  A(&act, M * ctx->F * es);
+  A((void **)&apart, chunk * per_row);
+  const size_t n_groups_total = (size_t)B * ((P + grp_rows - 1) / grp_rows);
+  const size_t tab_ints = M * 8 + n_groups_total * 4 + 4 * B + 64;
+  A((void **)&tab, tab_ints * 4);
+  auto cleanup = [&]() {
+    dfree(ctx, h); dfree(ctx, part); dfree(ctx, xb); dfree(ctx, q); dfree(ctx, att); dfree(ctx, act);
+    dfree(ctx, apart); dfree(ctx, tab);
+  };
+  if (st != DEX_OK) { cleanup(); return fail(ctx, st); }
+
+  // row tables: rows ordered (seq, position)
+  std::vector<int> host(tab_ints, 0);
+  int *t_seq = host.data(), *t_pos = t_seq + M, *t_entry = t_pos + M, *t_tok = t_entry + M, *t_nc = t_tok + M,
+      *t_coff = t_nc + M, *t_bnd = t_coff + M, *t_zero = t_bnd + M;
+  int *g_row0 = t_zero + M, *g_nrows = g_row0 + n_groups_total, *g_seq = g_nrows + n_groups_total;
+  int *g_rel = g_seq + n_groups_total;
+  int *ex_src = g_rel + n_groups_total, *ex_zero = ex_src + B, *ex_cidx = ex_zero + B;
+  for (int s = 0; s < B; ++s)
+    for (int p = 0; p < P; ++p) {
+      const size_t r = (size_t)s * P + p;
+      t_seq[r] = s; t_pos[r] = p; t_entry[r] = p; t_tok[r] = prompts[r]; t_nc[r] = p + 1;
+      t_coff[r] = 0; t_bnd[r] = 0; t_zero[r] = 0;
+    }
+  std::vector<int> gr0, gnr, gsq;
+  for (int s = 0; s < B; ++s)
+    for (int p = 0; p < P; p += grp_rows) {
+      gr0.push_back(s * P + p);
+      gnr.push_back(std::min(grp_rows, P - p));
+      gsq.push_back(s);
+    }
+  const int ng = (int)gr0.size();
+  std::copy(gr0.begin(), gr0.end(), g_row0);
+  std::copy(gnr.begin(), gnr.end(), g_nrows);
+  std::copy(gsq.begin(), gsq.end(), g_seq);
+  // attention chunks: runs of whole groups holding at most `chunk` rows
+  std::vector<std::array<int, 4>> chunks;   // first group, groups, first row, rows
+  for (int g = 0; g < ng;) {
+    const int c0 = gr0[g];
+    int e = g, rows_in = 0;
+    while (e < ng && (rows_in + gnr[e] <= (int)chunk || e == g)) { rows_in += gnr[e]; ++e; }
+    for (int i = g; i < e; ++i) g_rel[i] = gr0[i] - c0;
+    chunks.push_back({g, e - g, c0, rows_in});
+    g = e;
+  }
+  for (int s = 0; s < B; ++s) { ex_src[s] = s * P + P - 1; ex_zero[s] = 0; ex_cidx[s] = 0; }
+  HIPCHK(hipMemcpyAsync(tab, host.data(), tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
+  const int *d_seq = tab, *d_pos = tab + M, *d_entry = d_pos + M, *d_tok = d_entry + M, *d_nc = d_tok + M,
+            *d_coff = d_nc + M, *d_zero = d_coff + 2 * M;
+  const int *d_g0 = d_zero + M, *d_gn = d_g0 + n_groups_total, *d_gs = d_gn + n_groups_total;
+  const int *d_grel = d_gs + n_groups_total;
+  const int *d_exsrc = d_grel + n_groups_total, *d_exzero = d_exsrc + B;
+
+  {
+    PrepArgs p{};
+    p.M = (int)M; p.d = d; p.n_part = ctx->n_part; p.from_embed = 1; p.row_tok = d_tok; p.embed = ctx->embed;
+    p.g = (const float *)LW(ctx, 0, DEX_P_ATTN_NORM); p.h = h; p.part = part; p.xb = xb;
+    HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
+  }
+  const size_t layer_kv = (size_t)B * ctx->Hkv * ctx->E * hd * es;
+  for (int l = 0; l < ctx->L; ++l) {
+    const float alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_WQ); a.w1 = LW(ctx, l, DEX_P_WK); a.w2 = LW(ctx, l, DEX_P_WV);
+      a.n0 = H * hd; a.n1 = ctx->Hkv * hd; a.n2 = ctx->Hkv * hd;
+      a.N = (H + 2 * ctx->Hkv) * hd; a.K = d; a.x = xb; a.ldx = d; a.M = (int)M;
+      a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+      a.out = q; a.ld_out = H * hd;
+      a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
+      a.kv_entries = ctx->E; a.n_heads = H; a.n_kv_heads = ctx->Hkv; a.head_dim = hd;
+      a.row_seq = d_seq; a.row_pos = d_pos; a.row_entry = d_entry; a.rope = ctx->rope;
+      HIPCHK(launch_gemm(ctx->dtype, EPI_QKV, a, 1, ctx->stream));
+    }
+    for (const auto &ch : chunks) {
+      const int g_first = ch[0], g_cnt = ch[1], c0 = ch[2], cn = ch[3];
+      AttnArgs a{};
+      a.q = q + (size_t)c0 * H * hd; a.ldq = H * hd;
+      a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
+      a.kv_entries = ctx->E; a.n_kv_heads = ctx->Hkv; a.n_heads = H; a.head_dim = hd; a.batch = B;
+      a.grp_row0 = d_grel + g_first; a.grp_nrows = d_gn + g_first; a.grp_seq = d_gs + g_first;
+      a.row_pos = d_pos + c0; a.row_nc = d_nc + c0; a.row_chain_off = d_coff + c0; a.chain = d_zero;
+      a.part = apart; a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
+      HIPCHK(launch_attention(ctx->dtype, a, g_cnt, ctx->stream));
+      CombineArgs cb{};
+      cb.part = apart; cb.row_pos = d_pos + c0; cb.jmax = jmax; cb.n_heads = H; cb.head_dim = hd;
+      cb.out = (char *)att + (size_t)c0 * H * hd * es; cb.ld_out = H * hd;
+      HIPCHK(launch_combine(ctx->dtype, cb, cn, ctx->stream));
+    }
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_WO); a.n0 = d; a.N = d; a.K = H * hd; a.x = att; a.ldx = H * hd; a.M = (int)M;
+      a.h = h; a.ld_h = d; a.alpha = alpha; a.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM); a.xb = xb;
+      a.part_out = part; a.n_part_out = ctx->n_part;
+      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
+    }
+    {
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_W_GATE); a.w1 = LW(ctx, l, DEX_P_W_UP); a.n0 = ctx->F; a.N = ctx->F; a.K = d;
+      a.x = xb; a.ldx = d; a.M = (int)M; a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d;
+      a.eps = ctx->eps; a.act = act; a.ld_act = ctx->F;
+      HIPCHK(launch_gemm(ctx->dtype, EPI_SWIGLU, a, 1, ctx->stream));
+    }
+    {
+      const bool last = l == ctx->L - 1;
+      GemmArgs a{};
+      a.w0 = LW(ctx, l, DEX_P_W_DOWN); a.n0 = d; a.N = d; a.K = ctx->F; a.x = act; a.ldx = ctx->F; a.M = (int)M;
+      a.h = h; a.ld_h = d; a.alpha = alpha;
+      a.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
+      a.xb = last ? nullptr : xb; a.part_out = part; a.n_part_out = ctx->n_part;
+      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
+    }
+  }
+  // y_0: final-depth exit head at the last prompt position of every sequence
+  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr);
+  if (es2 != DEX_OK) { cleanup(); return fail(ctx, es2); }
+  HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, B * 4, hipMemcpyDeviceToHost, ctx->stream));
+  HIPCHK(hipStreamSynchronize(ctx->stream));
+  cleanup();
+  harvest_timing(ctx);
+  for (int s = 0; s < B; ++s) {
+    Seq &q2 = ctx->seqs[s];
+    q2.committed.assign(prompts + (size_t)s * P, prompts + (size_t)(s + 1) * P);
+    const int y0 = ctx->res_host[s];
+    q2.committed.push_back(y0);
+    first[s] = y0;
+    q2.slots.clear();
+    Slot a;
+    a.x = y0; a.pos = P; a.u.clear(); a.child.assign(ctx->N, -1);
+    q2.slots.push_back(a);
+    q2.half = 0;
+    q2.active = (int)q2.committed.size() < ctx->max_ctx;
+    q2.last_map.clear(); q2.last_fresh = -1; q2.last_committed_pos = -1;
+  }
+  ctx->prefilled = true;
+  ctx->rounds = 0;
+  return DEX_OK;
+}
+
+dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
+  if (!ctx) return DEX_E_INVAL;
+  if (ctx->poisoned) { ctx->err = "context poisoned by an earlier failure"; return DEX_E_STATE; }
+  if (!ctx->prefilled) { ctx->err = "dex_step before dex_prefill"; return DEX_E_STATE; }
+  if (!committed_out) { ctx->err = "committed is NULL"; return DEX_E_INVAL; }
+  const int N = ctx->N, B = ctx->B;
+  for (int s = 0; s < B; ++s) committed_out[s] = -1;
+  bool any = false;
+  for (auto &s : ctx->seqs) any |= s.active;
+  if (!any) { ctx->err = "every sequence reached max_context"; return DEX_E_CAPACITY; }
+
+  // ---------------------------------------------------------------- plan
+  std::vector<Row> rows;            // priority order within each sequence
+  std::vector<int> q_start(B, -1);
+  for (int si = 0; si < B; ++si) {
+    Seq &s = ctx->seqs[si];
+    if (!s.active) continue;
+    q_start[si] = s.slots[0].c;
+    std::vector<Item> items = plan_items(ctx, s);
+    for (const Item &it : items) {
+      if (it.kind == 0) {
+        rows.push_back({si, it.slot, s.slots[it.slot].c});
+      } else {
+        if ((int)s.slots.size() >= ctx->S) { ctx->err = "lattice slot capacity exceeded"; return fail(ctx, DEX_E_CAPACITY); }
+        Slot ns;
+        ns.x = s.slots[it.slot].u[it.f];
+        ns.pos = s.slots[it.slot].pos + 1;
+        ns.parent = it.slot;
+        ns.fork_stage = it.f;
+        ns.child.assign(N, -1);
+        s.slots.push_back(ns);
+        const int ni = (int)s.slots.size() - 1;
+        s.slots[it.slot].child[it.f] = ni;
+        rows.push_back({si, ni, 0});
+      }
+    }
+  }
+  // stage-major order, then sequence, then priority (stable)
+  std::stable_sort(rows.begin(), rows.end(), [](const Row &a, const Row &b) {
+    if (a.stage != b.stage) return a.stage < b.stage;
+    return a.seq < b.seq;
+  });
+  const int R = (int)rows.size();
+  if (R > ctx->R_max) { ctx->err = "round rows exceed capacity"; return fail(ctx, DEX_E_CAPACITY); }
+
+  // ------------------------------------------------------- row tables
+  int *T = ctx->tab_host;
+  int *t_seq = T, *t_pos = T + R, *t_entry = T + 2 * R, *t_bnd = T + 3 * R, *t_tok = T + 4 * R,
+      *t_nc = T + 5 * R, *t_coff = T + 6 * R, *t_maskn = T + 7 * R, *t_cidx = T + 8 * R;
+  int *t_mask = T + 9 * R;                 // [R][N]
+  int *t_chain = t_mask + R * N;           // [R * CH_MAX]
+  int *t_g0 = t_chain + R * ctx->CH_MAX;   // groups (stage-local row0), up to R
+  int *t_gn = t_g0 + R, *t_gs = t_gn + R;
+  int *t_commit = t_gs + R;                // [B] anchor candidate offsets of committing sequences
+  std::vector<int> stage_r0(N + 1, 0), stage_g0(N + 1, 0);
+  int chain_used = 0, ngroups = 0;
+  const int G = ctx->H / ctx->Hkv;
+  const int grp_rows = std::max(1, ATT_MAX_PAIRS / G);
+  for (int r = 0; r < R; ++r) {
+    const Row &rw = rows[r];
+    const Seq &s = ctx->seqs[rw.seq];
+    const Slot &sl = s.slots[rw.slot];
+    t_seq[r] = rw.seq;
+    t_pos[r] = sl.pos;
+    t_entry[r] = slot_entry(ctx, s, rw.slot);
+    t_bnd[r] = slot_global(ctx, rw.seq, s, rw.slot);
+    t_tok[r] = sl.x;
+    t_nc[r] = (int)s.committed.size() - 1;
+    t_coff[r] = chain_used;
+    std::vector<int> anc = ancestors(s, rw.slot);
+    if ((int)anc.size() + 1 > ctx->CH_MAX) { ctx->err = "lattice chain too deep"; return fail(ctx, DEX_E_CAPACITY); }
+    for (int a : anc) t_chain[chain_used++] = slot_entry(ctx, s, a);
+    t_chain[chain_used++] = slot_entry(ctx, s, rw.slot);
+    // DECS mask: tokens proposed by shallower nodes of this slot chain,
+    // except the anchor's final-depth node
+    int nm = 0;
+    if (ctx->decs && !(rw.slot == 0 && rw.stage == N - 1))
+      for (int j = 0; j < rw.stage; ++j) t_mask[r * N + nm++] = sl.u[j];
+    t_maskn[r] = nm;
+    t_cidx[r] = t_bnd[r] * N + rw.stage;
+    stage_r0[rw.stage + 1] = r + 1;
+  }
+  for (int k = 1; k <= N; ++k) stage_r0[k] = std::max(stage_r0[k], stage_r0[k - 1]);
+  // attention row groups per stage: consecutive rows of one sequence
+  for (int k = 0; k < N; ++k) {
+    stage_g0[k] = ngroups;
+    for (int r = stage_r0[k]; r < stage_r0[k + 1];) {
+      int e = r;
+      while (e < stage_r0[k + 1] && rows[e].seq == rows[r].seq && e - r < grp_rows) ++e;
+      t_g0[ngroups] = r - stage_r0[k];
+      t_gn[ngroups] = e - r;
+      t_gs[ngroups] = rows[r].seq;
+      ++ngroups;
+      r = e;
+    }
+  }
+  stage_g0[N] = ngroups;
+  std::vector<int> commit_seqs;
+  for (int si = 0; si < B; ++si) {
+    Seq &s = ctx->seqs[si];
+    if (s.active && s.slots[0].c == N - 1) {
+      t_commit[commit_seqs.size()] = slot_global(ctx, si, s, 0) * N;
+      commit_seqs.push_back(si);
+    }
+  }
+  const size_t tab_ints = (size_t)(t_commit - T) + commit_seqs.size() + 1;
+  if (tab_ints > ctx->tab_cap) { ctx->err = "row table overflow"; return fail(ctx, DEX_E_CAPACITY); }
+  HIPCHK(hipMemcpyAsync(ctx->tab_dev, T, tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
+  const int *D = ctx->tab_dev;
+  auto dptr = [&](const int *hp) { return D + (hp - T); };
+
+  // ------------------------------------------------------------ sweep
+  int layers_streamed = 0, row_layers = 0;
+  for (int k = 0; k < N; ++k) {
+    const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
+    if (M == 0) continue;
+    const std::vector<int> &ls = ctx->stage_layers[k];
+    layers_streamed += (int)ls.size();
+    row_layers += M * (int)ls.size();
+    StageTables t{};
+    t.seq = dptr(t_seq) + r0; t.pos = dptr(t_pos) + r0; t.entry = dptr(t_entry) + r0; t.bnd = dptr(t_bnd) + r0;
+    t.tok = dptr(t_tok) + r0; t.nc = dptr(t_nc) + r0; t.chain_off = dptr(t_coff) + r0; t.chain = dptr(t_chain);
+    t.g_row0 = dptr(t_g0) + stage_g0[k]; t.g_nrows = dptr(t_gn) + stage_g0[k]; t.g_seq = dptr(t_gs) + stage_g0[k];
+    t.n_groups = stage_g0[k + 1] - stage_g0[k];
+    {
+      PrepArgs p{};
+      p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
+      p.row_tok = t.tok; p.row_src = t.bnd; p.embed = ctx->embed; p.bnd_h = ctx->bnd_h; p.bnd_part = ctx->bnd_part;
+      p.g = (const float *)LW(ctx, ls.front(), DEX_P_ATTN_NORM);
+      p.h = ctx->h_w; p.part = ctx->part_w; p.xb = ctx->xb_w;
+      TimedLaunch tl(ctx, 7, 0.0);
+      HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
+    }
+    dex_status rs = run_layers(ctx, ls.front(), ls.back(), M, t, ctx->h_w, ctx->part_w, ctx->xb_w, ctx->q_w,
+                               ctx->att_w, ctx->act_w, ctx->attn_part, ctx->jmax, true, t.bnd);
+    if (rs != DEX_OK) return fail(ctx, rs);
+  }
+  // ---------------------------------------------------- exit + commit
+  dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),
+                           dptr(t_cidx), ctx->cand);
+  if (xs != DEX_OK) return fail(ctx, xs);
+  {
+    CommitArgs c{};
+    c.n = (int)commit_seqs.size(); c.seq_cand = dptr(t_commit); c.N = N; c.cand = ctx->cand; c.out = ctx->commit_dev;
+    HIPCHK(launch_commit(c, ctx->stream));
+  }
+  HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, R * 4, hipMemcpyDeviceToHost, ctx->stream));
+  if (!commit_seqs.empty())
+    HIPCHK(hipMemcpyAsync(ctx->res_host + R, ctx->commit_dev, commit_seqs.size() * 2 * 4, hipMemcpyDeviceToHost,
+                          ctx->stream));
+  HIPCHK(hipStreamSynchronize(ctx->stream));
+  harvest_timing(ctx);
+  ctx->rounds += 1;
+
+  // --------------------------------------------------- insert candidates
+  for (int r = 0; r < R; ++r) {
+    Slot &sl = ctx->seqs[rows[r].seq].slots[rows[r].slot];
+    sl.u.push_back(ctx->res_host[r]);
+    sl.c += 1;
+  }
+  if (info) {
+    std::memset(info, 0, sizeof(*info));
+    info->n_rows = R;
+    for (int r = 0; r < R && r < DEX_MAX_ROWS; ++r) {
+      info->rows_per_stage[rows[r].stage] += 1;
+      info->row_seq[r] = rows[r].seq;
+      info->row_slot[r] = rows[r].slot;
+      info->row_stage[r] = rows[r].stage;
+      info->row_pos[r] = ctx->seqs[rows[r].seq].slots[rows[r].slot].pos;
+      info->row_token[r] = ctx->res_host[r];
+    }
+    info->layers_streamed = layers_streamed;
+    info->row_layers = row_layers;
+    for (int s = 0; s < B; ++s) { info->q[s] = q_start[s]; info->kstar[s] = -1; }
+    info->rounds_total = ctx->rounds;
+  }
+  // ------------------------------------------------- commit + collapse
+  int njobs = 0;
+  int *J = ctx->job_host;
+  for (size_t ci = 0; ci < commit_seqs.size(); ++ci) {
+    const int si = commit_seqs[ci];
+    Seq &s = ctx->seqs[si];
+    const Slot A = s.slots[0];
+    const int y = ctx->res_host[R + 2 * ci], kstar = ctx->res_host[R + 2 * ci + 1];
+    // the host's own reading of the same rule must agree with the device
+    int kh = N - 1;
+    for (int j = 0; j < N - 1; ++j)
+      if (A.u[j] == A.u[N - 1]) { kh = j; break; }
+    if (A.c != N || y != A.u[N - 1] || kstar != kh) {
+      ctx->err = "commit mismatch between device and host lattice";
+      return fail(ctx, DEX_E_HIP);
+    }
+    committed_out[si] = y;
+    if (info) info->kstar[si] = kstar;
+    s.committed.push_back(y);
+    // old anchor's keys/values become committed position A.pos
+    J[6 * njobs + 0] = si; J[6 * njobs + 1] = slot_entry(ctx, s, 0); J[6 * njobs + 2] = A.pos;
+    J[6 * njobs + 3] = 0; J[6 * njobs + 4] = 0; J[6 * njobs + 5] = 0;
+    ++njobs;
+    const int child = (kstar <= N - 2) ? A.child[kstar] : -1;
+    std::vector<int> keep;
+    if (child >= 0) {
+      for (int i = 0; i < (int)s.slots.size(); ++i) {
+        int t = i;
+        while (t >= 0 && t != child) t = s.slots[t].parent;
+        if (t == child) keep.push_back(i);
+      }
+    }
+    const int nh = 1 - s.half;
+    std::vector<Slot> ns;
+    if (!keep.empty()) {
+      std::vector<int> remap(s.slots.size(), -1);
+      for (int j = 0; j < (int)keep.size(); ++j) remap[keep[j]] = j;
+      for (int j = 0; j < (int)keep.size(); ++j) {
+        Slot sl = s.slots[keep[j]];
+        sl.parent = (keep[j] == child) ? -1 : remap[sl.parent];
+        if (keep[j] == child) sl.fork_stage = -1;
+        for (int &ch : sl.child) ch = (ch >= 0) ? remap[ch] : -1;
+        ns.push_back(sl);
+        J[6 * njobs + 0] = si;
+        J[6 * njobs + 1] = ctx->max_ctx + s.half * ctx->S + keep[j];
+        J[6 * njobs + 2] = ctx->max_ctx + nh * ctx->S + j;
+        J[6 * njobs + 3] = s.half * ctx->S + keep[j];
+        J[6 * njobs + 4] = nh * ctx->S + j;
+        J[6 * njobs + 5] = 1;
+        ++njobs;
+      }
+    } else {
+      Slot f;
+      f.x = y; f.pos = A.pos + 1; f.child.assign(N, -1);
+      ns.push_back(f);
+    }
+    s.slots = ns;
+    s.half = nh;
+    s.last_map = keep;
+    s.last_fresh = keep.empty() ? 1 : 0;
+    s.last_committed_pos = A.pos;
+    if ((int)s.committed.size() >= ctx->max_ctx) s.active = false;
+  }
+  if (njobs > 0) {
+    HIPCHK(hipMemcpyAsync(ctx->job_dev, J, njobs * 6 * 4, hipMemcpyHostToDevice, ctx->stream));
+    CollapseArgs c{};
+    c.n_jobs = njobs; c.job = ctx->job_dev; c.kc = ctx->kc; c.vc = ctx->vc;
+    c.n_layers = ctx->L; c.batch = B; c.n_kv_heads = ctx->Hkv; c.kv_entries = ctx->E; c.head_dim = ctx->hd;
+    c.elem_bytes = ctx->es; c.bnd_h = ctx->bnd_h; c.bnd_part = ctx->bnd_part; c.cand = ctx->cand;
+    c.slots2 = 2 * ctx->S; c.d = ctx->d; c.n_part = ctx->n_part; c.N = N; c.max_ctx = ctx->max_ctx; c.S = ctx->S;
+    TimedLaunch tl(ctx, 7, 0.0);
+    HIPCHK(launch_collapse(c, ctx->stream));
+  }
+  return DEX_OK;
+}
+
+dex_status dex_debug_set_logits_tap(dex_ctx *ctx, float *buf, int32_t cap) {
+  if (!ctx) return DEX_E_INVAL;
+  if (buf && cap < ctx->R_max) { ctx->err = "logits tap capacity below rows per round"; return DEX_E_INVAL; }
+  ctx->logits_tap = buf;
+  ctx->logits_cap = cap;
+  return DEX_OK;
+}
+
+dex_status dex_debug_lattice(dex_ctx *ctx, int32_t seq, int32_t *out, int32_t cap, int32_t *n) {
+  if (!ctx || !out || !n || seq < 0 || seq >= ctx->B) return DEX_E_INVAL;
+  const Seq &s = ctx->seqs[seq];
+  *n = (int)s.slots.size();
+  if (cap < *n) { ctx->err = "slot table capacity too small"; return DEX_E_INVAL; }
+  const int st = 5 + ctx->N;
+  for (int i = 0; i < *n; ++i) {
+    const Slot &sl = s.slots[i];
+    int *o = out + i * st;
+    o[0] = sl.x; o[1] = sl.pos; o[2] = sl.parent; o[3] = sl.fork_stage; o[4] = sl.c;
+    for (int j = 0; j < ctx->N; ++j) o[5 + j] = j < (int)sl.u.size() ? sl.u[j] : -1;
+  }
+  return DEX_OK;
+}
+
+dex_status dex_debug_last_collapse(dex_ctx *ctx, int32_t seq, int32_t *map, int32_t cap, int32_t *n,
+                                   int32_t *fresh, int32_t *cpos) {
+  if (!ctx || !map || !n || !fresh || !cpos || seq < 0 || seq >= ctx->B) return DEX_E_INVAL;
+  const Seq &s = ctx->seqs[seq];
+  *n = (int)s.last_map.size();
+  if (cap < *n) return DEX_E_INVAL;
+  for (int i = 0; i < *n; ++i) map[i] = s.last_map[i];
+  *fresh = s.last_fresh;
+  *cpos = s.last_committed_pos;
+  return DEX_OK;
+}
+
+dex_status dex_debug_kv_layout(dex_ctx *ctx, void **k, void **v, int64_t *entries) {
+  if (!ctx || !k || !v || !entries) return DEX_E_INVAL;
+  *k = ctx->kc;
+  *v = ctx->vc;
+  *entries = ctx->E;
+  return DEX_OK;
+}
+
+dex_status dex_debug_slot_entry(dex_ctx *ctx, int32_t seq, int32_t slot, int32_t *entry) {
+  if (!ctx || !entry || seq < 0 || seq >= ctx->B) return DEX_E_INVAL;
+  if (slot < 0 || slot >= ctx->S) return DEX_E_INVAL;
+  *entry = slot_entry(ctx, ctx->seqs[seq], slot);
+  return DEX_OK;
+}
+
+dex_status dex_debug_set_kernel_timing(dex_ctx *ctx, int32_t enable) {
+  if (!ctx) return DEX_E_INVAL;
+  ctx->timing = enable != 0;
+  for (int i = 0; i < 8; ++i) { ctx->t_ms[i] = 0; ctx->t_n[i] = 0; ctx->t_bytes[i] = 0; }
+  return DEX_OK;
+}
+
+dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *launches, double *bytes) {
+  if (!ctx || n < 0 || n > 8) return DEX_E_INVAL;
+  for (int i = 0; i < n; ++i) {
+    if (ms) ms[i] = ctx->t_ms[i];
+    if (launches) launches[i] = ctx->t_n[i];
+    if (bytes) bytes[i] = ctx->t_bytes[i];
+  }
+  return DEX_OK;
+}
+
+dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M, float *y,
+                          void *stream) {
+  if (!W || !x || !y || N < 1 || K < 1 || M < 1 || M > 64) return DEX_E_INVAL;
+  if (dtype != DEX_F32 && dtype != DEX_BF16) return DEX_E_INVAL;
+  if (K % (dtype == DEX_BF16 ? 8 : 4)) return DEX_E_INVAL;
+  GemmArgs a{};
+  a.w0 = W; a.n0 = N; a.N = N; a.K = K; a.x = x; a.ldx = K; a.M = M; a.out = y; a.ld_out = N;
+  hipError_t e = launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
+  return e == hipSuccess ? DEX_OK : DEX_E_HIP;
+}
+
+dex_status dex_debug_copy(void *dst, const void *src, int64_t bytes, void *stream) {
+  if (!dst || !src || bytes < 0 || bytes % 16) return DEX_E_INVAL;
+  hipError_t e = launch_copy(dst, src, bytes, (hipStream_t)stream);
+  return e == hipSuccess ? DEX_OK : DEX_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,359 @@
+// Skinny-M matrix-core GEMM for the decode step on gfx950.
+//
+//   acc[m][n] = sum_k x[m][k] * W[n][k]          (W row-major [N][K])
+//
+// The M <= 64 rows of a round are tiny next to the weights, so the kernel is
+// a weight stream: one workgroup owns a 16-column tile of W (two tiles for
+// the gate/up pair), its eight waves split K by interleaved 16-byte steps,
+// and each wave issues 128-bit loads of W (A operand, 16 rows x 64 bytes per
+// instruction) and of x (B operand, from L2) into v_mfma_f32_16x16x32_bf16
+// (bf16) or v_mfma_f32_16x16x4_f32 (fp32) tiles.  Rows beyond M are zero.
+// The split-K partials meet in LDS and are summed in wave order, so a row's
+// result depends only on its own input: the same bits for any M, any
+// neighbouring rows and any position in the batch.
+//
+// Epilogues fuse the elementwise work of a transformer layer:
+//   QKV     RMSNorm scale (from the producer's sum-of-squares partials), RoPE
+//           on q and k, q to a float buffer, k and v to the key/value cache
+//           at each row's entry;
+//   RESID   h += alpha * acc, the next RMSNorm's input g*h in the matrix-core
+//           type, and per-16-column sum-of-squares partials of h;
+//   SWIGLU  SiLU(r*gate) * (r*up) for the interleaved gate/up tiles;
+//   LOGITS  r*acc, optional float logits tap, DECS mask (-inf), and the
+//           tile's argmax (lowest id on ties);
+//   PLAIN   float output (tests).
+#include "dex_kernels.h"
+
+namespace dex {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+
+__device__ __forceinline__ float bf2f(bf16 b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+template <typename T> __device__ __forceinline__ T to_t(float f);
+template <> __device__ __forceinline__ float to_t<float>(float f) { return f; }
+template <> __device__ __forceinline__ bf16 to_t<bf16>(float f) { return f2bf(f); }
+
+// One 16-byte fragment per lane and the MFMA steps it feeds.
+template <typename T> struct Frag;
+template <> struct Frag<bf16> {
+  u32x4_t v;
+  static constexpr int EPB = 8;           // elements per 16 bytes
+  __device__ __forceinline__ static f32x4_t mma(const Frag &a, const Frag &b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
+                                                   __builtin_bit_cast(bf16x8_t, b.v), c, 0, 0, 0);
+  }
+};
+template <> struct Frag<float> {
+  u32x4_t v;
+  static constexpr int EPB = 4;
+  __device__ __forceinline__ static f32x4_t mma(const Frag &a, const Frag &b, f32x4_t c) {
+    // k-slot (lane group g, element e) <-> k = 4 g + e, identical for A and B
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.x), __uint_as_float(b.v.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.y), __uint_as_float(b.v.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.z), __uint_as_float(b.v.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.w), __uint_as_float(b.v.w), c, 0, 0, 0);
+    return c;
+  }
+};
+
+__device__ __forceinline__ u32x4_t load16(const void *p, bool ok) {
+  if (!ok) return u32x4_t{0u, 0u, 0u, 0u};
+  return __builtin_nontemporal_load((const u32x4_t *)p);
+}
+__device__ __forceinline__ u32x4_t load16_cached(const void *p, bool ok) {
+  if (!ok) return u32x4_t{0u, 0u, 0u, 0u};
+  return *(const u32x4_t *)p;
+}
+
+// RMSNorm reciprocal scale of one row from its sum-of-squares partials.  The
+// single definition used by every consumer: lane j sums partials j, j+64, ...
+// in order, then a fixed butterfly across the wave.
+__device__ __forceinline__ float row_rscale(const float *part, int n_part, float inv_d, float eps, int lane) {
+  float s = 0.f;
+  for (int t = lane; t < n_part; t += 64) s += part[t];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  return 1.0f / sqrtf(s * inv_d + eps);
+}
+
+// Output column of local tile row r16 (0..15) for tile `tile`.  QKV tiles keep
+// the two RoPE partners (i, i + hd/2) of a head inside one tile.
+__device__ __forceinline__ int qkv_col(int tile, int r16, int hd) {
+  const int tph = hd / 16;                 // tiles per head
+  const int head = tile / tph, j = tile % tph;
+  const int dim = (r16 < 8) ? (8 * j + r16) : (hd / 2 + 8 * j + r16 - 8);
+  return head * hd + dim;
+}
+
+template <typename T, int EPI, int MB>
+__global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
+  using F = Frag<T>;
+  constexpr int EPB = F::EPB;
+  constexpr int KSTEP = 4 * EPB;               // k covered by one 16-byte step of a wave
+  constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;
+  constexpr int U = 4;                         // steps per prefetch chunk
+  __shared__ float red[GEMM_WAVES][NT][MB][64][4];
+  __shared__ float val[NT][16][16 * MB];
+  __shared__ float rs[16 * MB];
+
+  const int tile = blockIdx.x;
+  const int m0 = blockIdx.y * 16 * MB;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int Mloc = min(16 * MB, a.M - m0);
+
+  // ---- this lane's weight rows
+  const T *wrow[NT];
+  bool wok[NT];
+  {
+    int col;
+    if (EPI == EPI_QKV) col = qkv_col(tile, r16, a.head_dim);
+    else col = tile * 16 + r16;
+    if (EPI == EPI_SWIGLU) {
+      wok[0] = col < a.N;
+      wok[NT - 1] = col < a.N;
+      wrow[0] = (const T *)a.w0 + (size_t)(wok[0] ? col : 0) * a.K;
+      wrow[NT - 1] = (const T *)a.w1 + (size_t)(wok[0] ? col : 0) * a.K;
+    } else {
+      const T *base;
+      int r;
+      if (col < a.n0) { base = (const T *)a.w0; r = col; }
+      else if (col < a.n0 + a.n1) { base = (const T *)a.w1; r = col - a.n0; }
+      else { base = (const T *)a.w2; r = col - a.n0 - a.n1; }
+      wok[0] = col < a.N;
+      wrow[0] = base + (size_t)(wok[0] ? r : 0) * a.K;
+    }
+  }
+  // ---- this lane's activation rows (one per M block)
+  const T *xrow[MB];
+  bool xok[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = m0 + mb * 16 + r16;
+    xok[mb] = m < a.M;
+    xrow[mb] = (const T *)a.x + (size_t)(xok[mb] ? m : 0) * a.ldx;
+  }
+
+  f32x4_t acc[NT][MB];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nsteps = (a.K + KSTEP - 1) / KSTEP;
+  F wa[U][NT], xa[U][MB], wb[U][NT], xb[U][MB];
+
+  auto load_chunk = [&](int s0, F (&w)[U][NT], F (&x)[U][MB]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + u * GEMM_WAVES;
+      const int k = s * KSTEP + grp * EPB;
+      const bool kin = (s < nsteps) && (k < a.K);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) w[u][t].v = load16(wrow[t] + k, kin && wok[t]);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) x[u][mb].v = load16_cached(xrow[mb] + k, kin && xok[mb]);
+    }
+  };
+  auto compute_chunk = [&](const F (&w)[U][NT], const F (&x)[U][MB]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[t][mb] = F::mma(w[u][t], x[u][mb], acc[t][mb]);
+  };
+
+  int s = wave;
+  const int stride = U * GEMM_WAVES;
+  if (s < nsteps) load_chunk(s, wa, xa);
+  while (s < nsteps) {
+    const int sn = s + stride;
+    if (sn < nsteps) load_chunk(sn, wb, xb);
+    compute_chunk(wa, xa);
+    s = sn;
+    if (s >= nsteps) break;
+    const int sn2 = s + stride;
+    if (sn2 < nsteps) load_chunk(sn2, wa, xa);
+    compute_chunk(wb, xb);
+    s = sn2;
+  }
+
+  // ---- split-K partials meet in LDS, summed in wave order
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][t][mb][lane][i] = acc[t][mb][i];
+
+  // RMSNorm scales of this block's rows
+  if (a.part != nullptr) {
+    for (int ml = wave; ml < Mloc; ml += GEMM_WAVES) {
+      const float r = row_rscale(a.part + (size_t)(m0 + ml) * a.n_part, a.n_part, a.inv_d, a.eps, lane);
+      if (lane == 0) rs[ml] = r;
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < NT * MB * 256; e += GEMM_THREADS) {
+    const int t = e / (MB * 256), rem = e % (MB * 256);
+    const int mb = rem / 256, li = rem % 256;
+    const int ln = li >> 2, i = li & 3;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < GEMM_WAVES; ++w) sum += red[w][t][mb][ln][i];
+    // C layout: lane ln holds rows 4*(ln/16)+i (output columns) of column ln%16 (input rows)
+    const int nl = 4 * (ln >> 4) + i;
+    const int ml = mb * 16 + (ln & 15);
+    val[t][nl][ml] = sum;
+  }
+  __syncthreads();
+
+  // ---- epilogues
+  if constexpr (EPI == EPI_PLAIN) {
+    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 16, nl = e % 16;
+      const int n = tile * 16 + nl;
+      if (n < a.N) a.out[(size_t)(m0 + ml) * a.ld_out + n] = val[0][nl][ml];
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    const int hd = a.head_dim;
+    const int col0 = qkv_col(tile, 0, hd);       // first column of the tile
+    const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
+    const int j = tile % (hd / 16);
+    for (int e = threadIdx.x; e < 8 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 8, p = e % 8;           // pair p: dims 8j+p and hd/2+8j+p
+      const int m = m0 + ml;
+      const float r = (a.part != nullptr) ? rs[ml] : 1.f;
+      float x1 = val[0][p][ml] * r, x2 = val[0][p + 8][ml] * r;
+      const int i = 8 * j + p;
+      const int c1 = col0 - (col0 % hd) + i;    // column of dim i in this head
+      const int c2 = c1 + hd / 2;
+      if (c1 < nq + nk) {                        // q or k: rotate
+        const float2 cs = a.rope[(size_t)a.row_pos[m] * (hd / 2) + i];
+        const float y1 = x1 * cs.x - x2 * cs.y;
+        const float y2 = x2 * cs.x + x1 * cs.y;
+        x1 = y1;
+        x2 = y2;
+      }
+      if (c1 < nq) {
+        a.out[(size_t)m * a.ld_out + c1] = x1;
+        a.out[(size_t)m * a.ld_out + c2] = x2;
+      } else {
+        const bool isk = c1 < nq + nk;
+        const int cc = isk ? c1 - nq : c1 - nq - nk;
+        const int g = cc / hd, dim = cc % hd;
+        T *cache = (T *)(isk ? a.kc : a.vc);
+        const size_t base = (((size_t)a.row_seq[m] * a.n_kv_heads + g) * a.kv_entries + a.row_entry[m]) * hd;
+        cache[base + dim] = to_t<T>(x1);
+        cache[base + dim + hd / 2] = to_t<T>(x2);
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    __shared__ float sq[16][16 * MB];
+    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 16, nl = e % 16;
+      const int m = m0 + ml, n = tile * 16 + nl;
+      const float *hin = a.h + (size_t)m * a.ld_h;
+      float *hout = (a.row_bnd != nullptr) ? a.bnd_h + (size_t)a.row_bnd[m] * a.ld_h : a.h + (size_t)m * a.ld_h;
+      const float br = a.alpha * val[0][nl][ml];
+      const float hn = hin[n] + br;
+      hout[n] = hn;
+      if (a.xb != nullptr) ((T *)a.xb)[(size_t)m * a.ld_h + n] = to_t<T>(a.g_next[n] * hn);
+      sq[nl][ml] = hn * hn;
+    }
+    __syncthreads();
+    for (int ml = threadIdx.x; ml < Mloc; ml += GEMM_THREADS) {
+      const int m = m0 + ml;
+      float s = 0.f;
+#pragma unroll
+      for (int nl = 0; nl < 16; ++nl) s += sq[nl][ml];
+      float *po = (a.row_bnd != nullptr) ? a.bnd_part + (size_t)a.row_bnd[m] * a.n_part_out
+                                         : a.part_out + (size_t)m * a.n_part_out;
+      po[tile] = s;
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 16, nl = e % 16;
+      const int m = m0 + ml, n = tile * 16 + nl;
+      if (n >= a.N) continue;
+      const float r = (a.part != nullptr) ? rs[ml] : 1.f;
+      const float gt = val[0][nl][ml] * r, up = val[NT - 1][nl][ml] * r;
+      const float sg = gt / (1.0f + expf(-gt));
+      ((T *)a.act)[(size_t)m * a.ld_act + n] = to_t<T>(sg * up);
+    }
+  } else if constexpr (EPI == EPI_LOGITS) {
+    __shared__ float z[16][16 * MB];
+    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 16, nl = e % 16;
+      const int m = m0 + ml, n = tile * 16 + nl;
+      const float r = (a.part != nullptr) ? rs[ml] : 1.f;
+      float v = val[0][nl][ml] * r;
+      if (n < a.N) {
+        if (a.logits_tap != nullptr) a.logits_tap[(size_t)m * a.N + n] = v;
+        const int nm = a.mask_n[m];
+        for (int q = 0; q < nm; ++q)
+          if (a.mask_tok[(size_t)m * a.mask_stride + q] == n) v = -INFINITY;
+      } else {
+        v = -INFINITY;
+      }
+      z[nl][ml] = v;
+    }
+    __syncthreads();
+    for (int ml = threadIdx.x; ml < Mloc; ml += GEMM_THREADS) {
+      float best = -INFINITY;
+      int bi = -1;
+#pragma unroll
+      for (int nl = 0; nl < 16; ++nl) {
+        const float v = z[nl][ml];
+        if (v > best || bi < 0) { best = v; bi = tile * 16 + nl; }
+      }
+      a.amax[(size_t)(m0 + ml) * a.n_tiles + tile] = make_float2(best, __int_as_float(bi));
+    }
+  }
+}
+
+template <typename T, int EPI>
+static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
+  const int n_tiles = (a.N + 15) / 16;
+  dim3 block(GEMM_THREADS);
+  if (m_blocks <= 0) return hipErrorInvalidValue;
+  if (a.M <= 16) {
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 1>), dim3(n_tiles, 1), block, 0, s, a);
+  } else if (a.M <= 32) {
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 2>), dim3(n_tiles, 1), block, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 4>), dim3(n_tiles, (a.M + 63) / 64), block, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipStream_t s) {
+  if (dtype == 1) {
+    switch (epi) {
+      case EPI_PLAIN: return launch_t<bf16, EPI_PLAIN>(a, m_blocks, s);
+      case EPI_QKV: return launch_t<bf16, EPI_QKV>(a, m_blocks, s);
+      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, m_blocks, s);
+      case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, m_blocks, s);
+      case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, m_blocks, s);
+    }
+  } else {
+    switch (epi) {
+      case EPI_PLAIN: return launch_t<float, EPI_PLAIN>(a, m_blocks, s);
+      case EPI_QKV: return launch_t<float, EPI_QKV>(a, m_blocks, s);
+      case EPI_RESID: return launch_t<float, EPI_RESID>(a, m_blocks, s);
+      case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, m_blocks, s);
+      case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, m_blocks, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace dex

@@ -1,0 +1,86 @@
+"""The C-ABI library loads on a machine without a GPU, exports every symbol
+include/dex.h declares, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_29223_amd import dexlib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "dex.h")).read()
+    return sorted(set(re.findall(r"\b(dex_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(dexlib.LIB_PATH):
+        pytest.skip("libdex.so not built")
+    return dexlib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(names) == sorted(dexlib.EXPORTED)
+
+
+def _model(**kw):
+    m = dexlib.DexModel()
+    m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ffn, m.vocab = 4, 128, 4, 4, 32, 344, 512
+    m.rope_theta, m.rms_eps, m.residual_scale, m.weight_dtype = 1e4, 1e-5, 0.3, dexlib.DEX_F32
+    fake = ctypes.c_void_p(0x1000)
+    m.embed = m.final_norm = m.lm_head = 0x1000
+    arr = (ctypes.c_void_p * (4 * 9))(*([0x1000] * 36))
+    m.layers = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    for k, v in kw.items():
+        setattr(m, k, v)
+    return m, arr, fake
+
+
+def _config(X, W=0, B=1, ctxlen=64):
+    c = dexlib.DexConfig()
+    x = np.array(X, dtype=np.int32)
+    c.explored = x.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    c.n_explored, c.width_cap, c.decs, c.batch, c.max_context, c.hip_stream = len(X), W, 1, B, ctxlen, None
+    return c, x
+
+
+@pytest.mark.parametrize("X,W,B,msg", [
+    ([1, 2, 3], 0, 1, "last explored depth"),
+    ([2, 1, 4], 0, 1, "strictly increasing"),
+    ([0, 4], 0, 1, "strictly increasing"),
+    ([1, 2, 3, 4], 0, 64, "DEX_MAX_ROWS"),
+    ([4], -1, 1, "width_cap"),
+])
+def test_create_rejects_bad_explored_sets(lib, X, W, B, msg):
+    m, _a, _f = _model()
+    c, _x = _config(X, W, B)
+    ctx = ctypes.c_void_p()
+    st = lib.dex_create(ctypes.byref(m), ctypes.byref(c), ctypes.byref(ctx))
+    assert st == dexlib.DEX_E_INVAL
+    assert msg in lib.dex_last_error(None).decode()
+    assert not ctx.value
+
+
+def test_create_rejects_bad_dims(lib):
+    for kw in (dict(d_model=100), dict(head_dim=24), dict(n_kv_heads=3), dict(weight_dtype=7)):
+        m, _a, _f = _model(**kw)
+        c, _x = _config([4])
+        ctx = ctypes.c_void_p()
+        assert lib.dex_create(ctypes.byref(m), ctypes.byref(c), ctypes.byref(ctx)) == dexlib.DEX_E_INVAL
+
+
+def test_null_and_state_errors(lib):
+    assert lib.dex_step(None, None, None) == dexlib.DEX_E_INVAL
+    assert lib.dex_prefill(None, None, 0, None) == dexlib.DEX_E_INVAL
+    lib.dex_destroy(None)
+    assert lib.dex_debug_copy(None, None, 16, None) == dexlib.DEX_E_INVAL
+    assert lib.dex_debug_gemm(1, None, 16, 16, None, 1, None, None) == dexlib.DEX_E_INVAL

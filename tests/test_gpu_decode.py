@@ -1,0 +1,248 @@
+"""GPU: the DEX decode step through the C ABI against the oracle.
+
+  * DEX committed tokens are bit-identical to the GPU's own plain
+    autoregressive path (same library, X = {L}, width 1);
+  * tokens equal the oracle's greedy AR except where the oracle's top-2 gap
+    is below 1e-2 (teacher-forced: the oracle re-scores the GPU's prefix);
+  * every anchor row's exit logits (before the DECS mask) are within max
+    relative error 2e-2 of the oracle's at that depth and position;
+  * the lattice trace -- rows per round, commits, match depths, collapse
+    maps and slot tables -- equals the oracle lattice's on the same
+    candidate tokens, and (fp32 model) the oracle's own full DEX trace;
+  * the key/value collapse gather is bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ar, dex
+from oracle.lattice import Lattice
+from synth import configs, gen
+from tests.gpu_common import (LOGIT_RTOL, check_tokens_teacher_forced, decoder, host_weights,
+                              max_rel_err, torch_cuda)
+
+pytestmark = pytest.mark.gpu
+
+TINY = "tiny-4L-d128-fp32"
+SMALL = "small-12L-d768-bf16"
+
+
+def _run(dec, prompts, T, tap=None, collapse=True):
+    torch = torch_cuda()
+    B = dec.batch
+    first = dec.prefill(prompts)
+    toks = [[int(first[b])] for b in range(B)]
+    rounds = []
+    while min(len(t) for t in toks) < T:
+        c = dec.step()
+        inf = dec.info
+        rows = [(inf.row_seq[r], inf.row_slot[r], inf.row_stage[r], inf.row_pos[r], inf.row_token[r])
+                for r in range(inf.n_rows)]
+        rd = dict(rows=rows, kstar=[inf.kstar[b] for b in range(B)], committed=[int(x) for x in c],
+                  layers=inf.layers_streamed)
+        if tap is not None:
+            torch.cuda.synchronize()
+            rd["logits"] = tap[: inf.n_rows].cpu().numpy().copy()
+        if collapse:
+            rd["collapse"] = [dec.last_collapse(b) if c[b] >= 0 else None for b in range(B)]
+            rd["lattice"] = [dec.lattice(b) for b in range(B)]
+        rounds.append(rd)
+        for b in range(B):
+            if c[b] >= 0 and len(toks[b]) < T:
+                toks[b].append(int(c[b]))
+    return np.array(toks), rounds
+
+
+def _replay(rounds, N, W, decs, max_ctx, y0, P, seq=0):
+    """Feed the GPU's candidate tokens to the oracle lattice; every planning
+    and collapse decision must agree."""
+    lat = Lattice(N, W, bool(decs), max_ctx, int(y0), P)
+    for i, rd in enumerate(rounds):
+        if not any(r[0] == seq for r in rd["rows"]):
+            break
+        rows = lat.begin_round()
+        orc = [(lat.index(r.slot), r.stage, r.slot.pos) for r in rows]
+        order = sorted(range(len(orc)), key=lambda j: orc[j][1])
+        gpu = [(r[1], r[2], r[3], r[4]) for r in rd["rows"] if r[0] == seq]
+        assert [orc[j] for j in order] == [g[:3] for g in gpu], f"round {i}"
+        toks = [0] * len(rows)
+        for k, j in enumerate(order):
+            toks[j] = gpu[k][3]
+        cm = lat.end_round(rows, toks)
+        assert (cm is not None) == (rd["kstar"][seq] >= 0), f"round {i}"
+        if cm is not None:
+            assert cm.kstar == rd["kstar"][seq] and cm.token == rd["committed"][seq]
+            gmap, gfresh, gpos = rd["collapse"][seq]
+            assert list(cm.collapse_map) == list(gmap) and int(cm.fresh_anchor) == gfresh
+            assert gpos == cm.old_anchor.pos
+        tab = rd["lattice"][seq]
+        assert len(tab) == len(lat.slots)
+        for j, s in enumerate(lat.slots):
+            par = lat.index(s.parent) if s.parent is not None else -1
+            row = [s.x, s.pos, par, s.fork_stage, s.c] + (s.u + [-1] * (N - len(s.u)))
+            assert list(tab[j]) == row, f"round {i} slot {j}"
+    return lat
+
+
+@pytest.fixture(scope="module")
+def tiny_oracle():
+    cfg, w = host_weights(TINY)
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    prompt = [int(t) for t in gen.prompts(cfg)[0]]
+    pf = m.prefill(prompt)
+    return cfg, m, prompt, pf
+
+
+def test_tiny_dex_equals_ar_and_oracle(tiny_oracle):
+    torch = torch_cuda()
+    cfg, m, prompt, pf = tiny_oracle
+    T = cfg["gen_len"]
+    P = len(prompt)
+    ar_dec = decoder(TINY, explored=[cfg["n_layers"]], width_cap=1)
+    ar_toks, ar_rounds = _run(ar_dec, [prompt], T, collapse=False)
+    ar_dec.close()
+    dec = decoder(TINY)
+    tap = torch.empty((dec.batch * 8, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    toks, rounds = _run(dec, [prompt], T, tap=tap)
+    dec.close()
+    assert np.array_equal(toks, ar_toks)
+    assert all(len(r["rows"]) == 1 for r in ar_rounds)
+    # oracle: teacher-forced final-depth logits and exit logits on the GPU's prefix
+    seq = [int(t) for t in toks[0]]
+    X = cfg["explored"]
+    z = ar.depth_logits(m, prompt, seq, X, prefill=pf)
+    check_tokens_teacher_forced(z[:, -1], seq)
+    assert seq == ar.ar_generate(m, prompt, T, prefill=pf)
+    worst = 0.0
+    for rd in rounds:
+        for r, (s, slot, stage, pos, tok) in enumerate(rd["rows"]):
+            if slot != 0:
+                continue
+            t = pos + 1 - P
+            worst = max(worst, max_rel_err(rd["logits"][r], z[t - 1, stage]))
+    assert worst <= LOGIT_RTOL
+    assert worst < 1e-4          # fp32 model: agreement at float32 level
+    # trace: the oracle lattice on the GPU's tokens, then the oracle's own run
+    _replay(rounds, len(X), cfg["width_cap"], cfg["decs"], P + T, seq[0], P)
+    res = dex.dex_generate(m, prompt, X, cfg["width_cap"], True, T, prefill=pf)
+    assert res.tokens == seq
+    assert res.rounds == len(rounds)
+    for tr, rd in zip(res.trace, rounds):
+        orc = sorted([(a[1], a[0], a[2], tk) for a, tk in zip(tr.rows, tr.tokens)], key=lambda v: v[0])
+        gpu = [(st, sl, p, tk) for (_, sl, st, p, tk) in rd["rows"]]
+        assert orc == gpu
+        if tr.commit is not None:
+            assert tr.commit[1] == rd["kstar"][0] and tr.commit[2] == list(rd["collapse"][0][0])
+
+
+@pytest.mark.parametrize("X,W,decs", [([1, 2, 3, 4], 0, 0), ([1, 2, 3, 4], 3, 1), ([2, 4], 0, 1),
+                                      ([1, 3, 4], 2, 0)])
+def test_tiny_variants_lossless_and_trace(tiny_oracle, X, W, decs):
+    cfg, m, prompt, pf = tiny_oracle
+    T = 40
+    P = len(prompt)
+    ar_dec = decoder(TINY, explored=[4], width_cap=1, max_context=P + T)
+    ar_toks, _ = _run(ar_dec, [prompt], T, collapse=False)
+    ar_dec.close()
+    dec = decoder(TINY, explored=X, width_cap=W, decs=decs, max_context=P + T)
+    toks, rounds = _run(dec, [prompt], T)
+    dec.close()
+    assert np.array_equal(toks, ar_toks)
+    _replay(rounds, len(X), W, decs, P + T, toks[0][0], P)
+    res = dex.dex_generate(m, prompt, X, W, bool(decs), T, prefill=pf, keep_trace=False)
+    assert res.tokens == [int(t) for t in toks[0]] and res.rounds == len(rounds)
+
+
+def test_tiny_batch_of_lattices_matches_single():
+    cfg = configs.get(TINY)
+    prompts = np.stack([gen.tokens(gen.mix64(s), cfg["prompt_len"], cfg["vocab"]) for s in (11, 12, 13)])
+    T = 24
+    dec = decoder(TINY, batch=3, max_context=cfg["prompt_len"] + T)
+    toks, rounds = _run(dec, prompts, T)
+    dec.close()
+    for b in range(3):
+        one = decoder(TINY, batch=1, max_context=cfg["prompt_len"] + T)
+        t1, r1 = _run(one, prompts[b:b + 1], T)
+        one.close()
+        assert np.array_equal(toks[b], t1[0])
+        _replay(rounds, 4, 0, 1, cfg["prompt_len"] + T, toks[b][0], cfg["prompt_len"], seq=b)
+
+
+def _snapshot(dec, torch):
+    from paper_2606_29223_amd import dexlib
+    k, v, E = dec.kv_layout()
+    cfg = dec.cfg
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    nbytes = cfg["n_layers"] * dec.batch * cfg["n_kv_heads"] * E * cfg["head_dim"] * es
+    out = []
+    for base in (k, v):
+        buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        assert dexlib.load().dex_debug_copy(buf.data_ptr(), base, nbytes, dec.stream.cuda_stream) == 0
+        torch.cuda.synchronize()
+        out.append(buf.cpu().numpy().view(np.uint16 if es == 2 else np.uint32).reshape(
+            cfg["n_layers"], dec.batch, cfg["n_kv_heads"], E, cfg["head_dim"]))
+    return out
+
+
+@pytest.mark.parametrize("name", [TINY, SMALL])
+def test_kv_collapse_gather_bitexact(name):
+    torch = torch_cuda()
+    cfg, _ = host_weights(name)
+    P = 24
+    prompt = gen.prompts(cfg)[:, :P]
+    dec = decoder(name, max_context=P + 40)
+    dec.prefill(prompt)
+    checked = 0
+    for _ in range(30):
+        before_k, before_v = _snapshot(dec, torch)
+        lat_before = dec.lattice(0)
+        entries = [dec.slot_entry(0, j) for j in range(len(lat_before))]
+        c = dec.step()
+        after_k, after_v = _snapshot(dec, torch)
+        if c[0] < 0:
+            continue
+        keep, fresh, cpos = dec.last_collapse(0)
+        new_entries = [dec.slot_entry(0, j) for j in range(len(keep))]
+        # the anchor's keys/values (entry of slot 0 before the step, as written
+        # during the step) land on committed position cpos
+        anchor_e = entries[0]
+        for (bk, ak) in ((before_k, after_k), (before_v, after_v)):
+            assert np.array_equal(ak[:, 0, :, cpos, :], ak[:, 0, :, anchor_e, :])
+            assert np.array_equal(ak[:, 0, :, :cpos, :], bk[:, 0, :, :cpos, :])   # older positions untouched
+            for j, old in enumerate(keep):
+                assert np.array_equal(ak[:, 0, :, new_entries[j], :], ak[:, 0, :, entries[old], :])
+        checked += 1
+    dec.close()
+    assert checked >= 5
+
+
+def test_small_bf16_lossless_and_oracle():
+    torch = torch_cuda()
+    cfg, w = host_weights(SMALL)
+    P = cfg["prompt_len"]
+    T = 48
+    prompt = gen.prompts(cfg)
+    ar_dec = decoder(SMALL, explored=[cfg["n_layers"]], width_cap=1, max_context=P + T)
+    ar_toks, _ = _run(ar_dec, prompt, T, collapse=False)
+    ar_dec.close()
+    dec = decoder(SMALL, max_context=P + T)
+    tap = torch.empty((4, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    toks, rounds = _run(dec, prompt, T, tap=tap)
+    dec.close()
+    assert np.array_equal(toks, ar_toks)
+    _replay(rounds, 4, cfg["width_cap"], 1, P + T, toks[0][0], P)
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    seq = [int(t) for t in toks[0]]
+    pl = [int(t) for t in prompt[0]]
+    pf = m.prefill(pl)
+    z = ar.depth_logits(m, pl, seq, cfg["explored"], prefill=pf)
+    flips = check_tokens_teacher_forced(z[:, -1], seq)
+    assert len(flips) <= 2
+    worst = 0.0
+    for rd in rounds:
+        for r, (s, slot, stage, pos, tok) in enumerate(rd["rows"]):
+            if slot == 0:
+                worst = max(worst, max_rel_err(rd["logits"][r], z[pos - P, stage]))
+    assert worst <= LOGIT_RTOL, worst
