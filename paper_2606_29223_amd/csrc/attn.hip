@@ -7,13 +7,16 @@
 // and its own slot, listed in `chain`.  Grouped-query heads: query head h
 // reads key/value head h / (H / Hkv).
 //
-// Work split: one workgroup per (row group, kv head, split of 256 logical
-// keys).  A row group is up to 64 / (H/Hkv) rows of one sequence; the
-// committed keys of a 64-key tile are staged in LDS once and shared by all
-// rows and all query heads of the group.  Each wave owns (row, head) pairs;
-// a lane owns one key of the tile for the scores and head dimensions lane
-// and lane + 64 for the value sum.  Online softmax across the split's tiles,
-// then a separate combine over splits.
+// Work split: one wave per (row group, kv head, split of 64 logical keys).
+// A row group is consecutive rows of one sequence.  Lane i holds the
+// committed key at position s0 + i in registers (loaded once, shared by every
+// row and query head of the group) and the split's committed values are
+// staged in LDS; a row whose logical key at that position lives in a lattice
+// slot reads it from its chain instead.  Per row: the G query heads' scores
+// run as independent FMA chains over the head dimensions, softmax statistics
+// are wave reductions, and lane i accumulates value dimensions
+// [i*hd/64, (i+1)*hd/64) over the split's keys in position order.  Each split
+// writes (o, max, sum) partials; a second kernel combines the splits.
 //
 // Every quantity a row computes depends only on its logical key sequence:
 // split and tile boundaries are fixed logical positions, each dot product
@@ -21,13 +24,11 @@
 // whether the key is read from LDS or from a chain entry, and the combine
 // walks splits in order.  So a node evaluated speculatively (tail keys in
 // lattice slots) gets the bits plain decoding gets at the same position.
+// Splits of 64 keys keep a long context spread over many waves: 8192 keys x
+// 8 kv heads x 8 sequences is 9216 waves per layer.
 #include "dex_kernels.h"
 
 namespace dex {
-
-__device__ __forceinline__ float ld_elem(const float *p) { return *p; }
-__device__ __forceinline__ float ld_elem(const bf16 *p) { return __uint_as_float(((uint32_t)*p) << 16); }
-__device__ __forceinline__ float bfl(bf16 b) { return __uint_as_float(((uint32_t)b) << 16); }
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -40,149 +41,277 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-template <typename T>
+// Element e of a packed row held as 32-bit words (bf16 pairs or floats).
+template <typename T> __device__ __forceinline__ float unpack(const uint32_t *w, int e);
+template <> __device__ __forceinline__ float unpack<bf16>(const uint32_t *w, int e) {
+  const uint32_t u = w[e >> 1];
+  return __uint_as_float((e & 1) ? (u & 0xffff0000u) : (u << 16));
+}
+template <> __device__ __forceinline__ float unpack<float>(const uint32_t *w, int e) { return __uint_as_float(w[e]); }
+
+// One wave per (row group, kv head, split of 64 logical keys).  Lane i owns
+// key s0 + i for the scores and head dimensions [i*DPL, i*DPL + DPL) for the
+// value sum.
+template <typename T, int HD>
 __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
-  constexpr int PAD = (sizeof(T) == 2) ? 2 : 1;    // odd word stride per LDS row
-  __shared__ float qs[ATT_MAX_PAIRS][128];
-  __shared__ T ks[ATT_TILE][128 + PAD];
-  __shared__ T vs[ATT_TILE][128 + PAD];
+  constexpr int WORDS = HD * (int)sizeof(T) / 4;     // 32-bit words per key row
+  constexpr int V4 = WORDS / 4;                      // 16-byte loads per key row
+  constexpr int DPL = HD >= 64 ? HD / 64 : 1;        // value dims per lane
+  constexpr int GMAX = 8;
+  constexpr int KSTRIDE = WORDS + 4;
+  constexpr int EPC = 16 / (int)sizeof(T);           // elements per 16-byte chunk
+  __shared__ __attribute__((aligned(16))) float qs[GMAX][HD];
+  __shared__ __attribute__((aligned(16))) uint32_t ks[ATT_SPLIT][KSTRIDE];
+  __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_SPLIT][WORDS];
+  __shared__ __attribute__((aligned(16))) float es[GMAX][ATT_SPLIT];
 
   const int gi = blockIdx.x, kvh = blockIdx.y, split = blockIdx.z;
   const int r0 = a.grp_row0[gi], nr = a.grp_nrows[gi], seq = a.grp_seq[gi];
-  const int hd = a.head_dim;
   const int G = a.n_heads / a.n_kv_heads;
-  const int npairs = nr * G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-
+  const int lane = threadIdx.x;
   int maxpos = 0, ncmax = 0;
   for (int r = 0; r < nr; ++r) {
     maxpos = max(maxpos, a.row_pos[r0 + r]);
     ncmax = max(ncmax, a.row_nc[r0 + r]);
   }
-  const int kbeg = split * ATT_SPLIT;
-  if (kbeg > maxpos) return;
-  const int kend = min(kbeg + ATT_SPLIT, maxpos + 1);
+  const int s0 = split * ATT_SPLIT;
+  if (s0 > maxpos) return;
+  const T *kbase = (const T *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const T *vbase = (const T *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
 
-  // queries of the group's pairs (pair p: row p / G, head kvh * G + p % G)
-  for (int e = threadIdx.x; e < npairs * hd; e += ATT_THREADS) {
-    const int p = e / hd, i = e % hd;
-    const int r = r0 + p / G, h = kvh * G + p % G;
-    qs[p][i] = a.q[(size_t)r * a.ldq + h * hd + i];
-  }
-
-  const T *kbase = (const T *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * hd;
-  const T *vbase = (const T *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * hd;
-
-  // per-pair running state (pairs p = wave, wave + 4, ...)
-  constexpr int PPW = ATT_MAX_PAIRS / 4;
-  float m_run[PPW], l_run[PPW], o0[PPW], o1[PPW];
+  // this lane's key lives in its own LDS row: the committed one at position t
+  // (shared by the rows of the group) or a row's chain entry; `held` names
+  // which one is there
+  const int t = s0 + lane;
+  uint4 *krow = (uint4 *)&ks[lane][0];
+  int held = -1;
+  // committed values of the split in LDS; the rest zero until a row's chain
+  // entries are patched in
+  const int tn = max(0, min(ATT_SPLIT, ncmax - s0));
+  {
+    constexpr int PER = ATT_SPLIT * V4 / ATT_THREADS;   // 16-byte loads per lane
+    uint4 v[PER];
 #pragma unroll
-  for (int i = 0; i < PPW; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; o0[i] = 0.f; o1[i] = 0.f; }
-
-  for (int t0 = kbeg; t0 < kend; t0 += ATT_TILE) {
-    __syncthreads();
-    // stage committed keys/values [t0, t0 + 64) that exist for some row
-    const int tn = max(0, min(ATT_TILE, ncmax - t0));
-    for (int e = threadIdx.x; e < tn * hd; e += ATT_THREADS) {
-      const int i = e / hd, c = e % hd;
-      ks[i][c] = kbase[(size_t)(t0 + i) * hd + c];
-      vs[i][c] = vbase[(size_t)(t0 + i) * hd + c];
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane + i * ATT_THREADS, j = e / V4, c = e % V4;
+      v[i] = (j < tn) ? ((const uint4 *)(vbase + (size_t)(s0 + j) * HD))[c] : make_uint4(0, 0, 0, 0);
     }
-    __syncthreads();
 #pragma unroll
-    for (int pi = 0; pi < PPW; ++pi) {
-      const int p = wave + 4 * pi;
-      if (p >= npairs) break;
-      const int r = r0 + p / G;
-      const int pos = a.row_pos[r], nc = a.row_nc[r];
-      if (t0 > pos) continue;
-      const int coff = a.row_chain_off[r];
-      // score of key t0 + lane
-      const int t = t0 + lane;
-      float s = -INFINITY;
-      if (t <= pos) {
-        const T *kp = (t < nc) ? &ks[lane][0] : kbase + (size_t)a.chain[coff + (t - nc)] * hd;
-        float acc = 0.f;
-        for (int i = 0; i < hd; ++i) acc = fmaf(qs[p][i], ld_elem(kp + i), acc);
-        s = acc * a.scale;
-      }
-      const float mt = wave_max(s);
-      const float mn = fmaxf(m_run[pi], mt);
-      const float c = expf(m_run[pi] - mn);
-      const float e = (t <= pos) ? expf(s - mn) : 0.f;
-      l_run[pi] = l_run[pi] * c + wave_sum(e);
-      float a0 = o0[pi] * c, a1 = o1[pi] * c;
-      const int nk = min(ATT_TILE, pos + 1 - t0);
-      for (int j = 0; j < nk; ++j) {
-        const float ej = __shfl(e, j, 64);
-        const int tj = t0 + j;
-        const T *vp = (tj < nc) ? &vs[j][0] : vbase + (size_t)a.chain[coff + (tj - nc)] * hd;
-        if (lane < hd) a0 = fmaf(ej, ld_elem(vp + lane), a0);
-        if (lane + 64 < hd) a1 = fmaf(ej, ld_elem(vp + lane + 64), a1);
-      }
-      o0[pi] = a0;
-      o1[pi] = a1;
-      m_run[pi] = mn;
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane + i * ATT_THREADS;
+      *((uint4 *)&vs[e / V4][0] + e % V4) = v[i];
     }
   }
-  // partials: o[hd], m, l
+
+  for (int rr = 0; rr < nr; ++rr) {
+    const int r = r0 + rr;
+    const int pos = a.row_pos[r], nc = a.row_nc[r], coff = a.row_chain_off[r];
+    if (s0 > pos) continue;
+    __syncthreads();
+    {
+      const float4 *qsrc = (const float4 *)(a.q + (size_t)r * a.ldq + kvh * G * HD);
+      float4 *qdst = (float4 *)&qs[0][0];
+      constexpr int Q4 = GMAX * HD / 4 / ATT_THREADS;
+      float4 qv[Q4];
 #pragma unroll
-  for (int pi = 0; pi < PPW; ++pi) {
-    const int p = wave + 4 * pi;
-    if (p >= npairs) break;
-    const int r = r0 + p / G, h = kvh * G + p % G;
-    if (a.row_pos[r] < kbeg) continue;
-    float *dst = a.part + (((size_t)r * a.n_heads + h) * a.jmax + split) * (hd + 2);
-    if (lane < hd) dst[lane] = o0[pi];
-    if (lane + 64 < hd) dst[lane + 64] = o1[pi];
-    if (lane == 0) { dst[hd] = m_run[pi]; dst[hd + 1] = l_run[pi]; }
+      for (int i = 0; i < Q4; ++i) {
+        const int e = lane + i * ATT_THREADS;
+        qv[i] = (e < G * HD / 4) ? qsrc[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < Q4; ++i) qdst[lane + i * ATT_THREADS] = qv[i];
+    }
+    // this row's chain values at positions [max(nc, s0), pos] of the split
+    const int tb = max(nc, s0), te = min(pos, s0 + ATT_SPLIT - 1);
+    for (int e = lane; e < (te - tb + 1) * V4; e += ATT_THREADS) {
+      const int tj = tb + e / V4, c = e % V4;
+      *((uint4 *)&vs[tj - s0][0] + c) = ((const uint4 *)(vbase + (size_t)a.chain[coff + (tj - nc)] * HD))[c];
+    }
+    // this row's key at logical position t: committed, or its own chain
+    const bool valid = t <= pos;
+    const int want = (t < nc) ? -2 : (valid ? a.chain[coff + (t - nc)] : -1);
+    if (want != -1 && want != held) {
+      const uint4 *src = (const uint4 *)(kbase + (size_t)(want == -2 ? t : want) * HD);
+#pragma unroll
+      for (int i = 0; i < V4; ++i) krow[i] = src[i];
+      held = want;
+    }
+    __syncthreads();
+    // scores, one independent chain per head, dimensions in order
+    float sacc[GMAX];
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g) sacc[g] = 0.f;
+#pragma unroll 2
+    for (int c = 0; c < V4; ++c) {
+      const uint4 kw = valid ? krow[c] : make_uint4(0, 0, 0, 0);
+      const uint32_t w4[4] = {kw.x, kw.y, kw.z, kw.w};
+      float kv[EPC];
+#pragma unroll
+      for (int e2 = 0; e2 < EPC; ++e2) kv[e2] = unpack<T>(w4, e2);
+#pragma unroll
+      for (int g = 0; g < GMAX; ++g) {
+        if (g < G) {
+          const float4 *q4 = (const float4 *)&qs[g][c * EPC];
+#pragma unroll
+          for (int e4 = 0; e4 < EPC / 4; ++e4) {
+            const float4 qv = q4[e4];
+            sacc[g] = fmaf(qv.x, kv[4 * e4 + 0], sacc[g]);
+            sacc[g] = fmaf(qv.y, kv[4 * e4 + 1], sacc[g]);
+            sacc[g] = fmaf(qv.z, kv[4 * e4 + 2], sacc[g]);
+            sacc[g] = fmaf(qv.w, kv[4 * e4 + 3], sacc[g]);
+          }
+        }
+      }
+    }
+    float m[GMAX], l[GMAX];
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g) {
+      if (g >= G) break;
+      const float sc = valid ? sacc[g] * a.scale : -INFINITY;
+      m[g] = wave_max(sc);
+      const float e = valid ? expf(sc - m[g]) : 0.f;
+      l[g] = wave_sum(e);
+      es[g][lane] = e;
+    }
+    __syncthreads();
+    // value sum over the split's 64 keys in position order (weights of keys
+    // past pos are exactly zero and their values finite)
+    float o[GMAX][DPL];
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g)
+#pragma unroll
+      for (int q = 0; q < DPL; ++q) o[g][q] = 0.f;
+    const int d0 = lane * DPL;
+    const bool dims_ok = d0 < HD;
+    const int dsafe = dims_ok ? d0 : 0;
+#pragma unroll 4
+    for (int j0 = 0; j0 < ATT_SPLIT; j0 += 4) {
+      float v[4][DPL];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int q = 0; q < DPL; ++q) v[jj][q] = unpack<T>(&vs[j0 + jj][0], dsafe + q);
+#pragma unroll
+      for (int g = 0; g < GMAX; ++g) {
+        if (g >= G) break;
+        const float4 e4 = *(const float4 *)&es[g][j0];
+        const float ev[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+          for (int q = 0; q < DPL; ++q) o[g][q] = fmaf(ev[jj], v[jj][q], o[g][q]);
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g) {
+      if (g >= G) break;
+      float *dst = a.part + (((size_t)r * a.n_heads + kvh * G + g) * a.jmax + split) * (HD + 2);
+      if (dims_ok) {
+#pragma unroll
+        for (int q = 0; q < DPL; ++q) dst[d0 + q] = o[g][q];
+      }
+      if (lane == 0) { dst[HD] = m[g]; dst[HD + 1] = l[g]; }
+    }
   }
+
 }
 
-
-// out[r][h] = sum_j e^{m_j - M} o_j / sum_j e^{m_j - M} l_j over the splits
-// j = 0 .. pos/256 of row r, in split order.
-template <typename T>
-__global__ __launch_bounds__(128) void combine_kernel(CombineArgs a) {
-  const int r = blockIdx.x, h = blockIdx.y, i = threadIdx.x;
-  const int hd = a.head_dim;
+// out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M}, M = max_j m_j,
+// over the splits j = 0 .. pos/64 of row r.  One wave per (row, head): lanes
+// over splits for the statistics (fixed butterflies), lanes over head
+// dimensions for the weighted sum, which runs over the splits in order.
+template <typename T, int HD>
+__global__ __launch_bounds__(64) void combine_kernel(CombineArgs a) {
+  constexpr int DPL = HD >= 64 ? HD / 64 : 1;
+  __shared__ float ws[ATT_MAX_SPLITS];
+  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
-  const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (hd + 2);
+  const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (HD + 2);
   float M = -INFINITY;
-  for (int j = 0; j < nsplit; ++j) M = fmaxf(M, src[j * (hd + 2) + hd]);
-  float o = 0.f, l = 0.f;
-  for (int j = 0; j < nsplit; ++j) {
-    const float w = expf(src[j * (hd + 2) + hd] - M);
-    l = fmaf(w, src[j * (hd + 2) + hd + 1], l);
-    if (i < hd) o = fmaf(w, src[j * (hd + 2) + i], o);
+  for (int j0 = 0; j0 < nsplit; j0 += 64) {
+    const int j = j0 + lane;
+    M = fmaxf(M, j < nsplit ? src[(size_t)j * (HD + 2) + HD] : -INFINITY);
   }
-  if (i < hd) {
-    const float v = o / l;
-    T *out = (T *)a.out + (size_t)r * a.ld_out + h * hd + i;
+  M = wave_max(M);
+  float lsum = 0.f;
+  for (int j0 = 0; j0 < nsplit; j0 += 64) {
+    const int j = j0 + lane;
+    float w = 0.f, lj = 0.f;
+    if (j < nsplit) {
+      w = expf(src[(size_t)j * (HD + 2) + HD] - M);
+      lj = src[(size_t)j * (HD + 2) + HD + 1];
+      ws[j] = w;
+    }
+    lsum += wave_sum(w * lj);
+  }
+  __syncthreads();
+  const int d0 = lane * DPL;
+  if (d0 >= HD) return;
+  float o[DPL];
+#pragma unroll
+  for (int q = 0; q < DPL; ++q) o[q] = 0.f;
+  for (int j0 = 0; j0 < nsplit; j0 += 8) {
+    float v[8][DPL];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+#pragma unroll
+      for (int q = 0; q < DPL; ++q)
+        v[jj][q] = (j0 + jj < nsplit) ? src[(size_t)(j0 + jj) * (HD + 2) + d0 + q] : 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      if (j0 + jj >= nsplit) break;
+      const float w = ws[j0 + jj];
+#pragma unroll
+      for (int q = 0; q < DPL; ++q) o[q] = fmaf(w, v[jj][q], o[q]);
+    }
+  }
+  T *out = (T *)a.out + (size_t)r * a.ld_out + h * HD + d0;
+#pragma unroll
+  for (int q = 0; q < DPL; ++q) {
+    const float v = o[q] / lsum;
     if constexpr (sizeof(T) == 2) {
       uint32_t u = __float_as_uint(v);
       u += 0x7fffu + ((u >> 16) & 1u);
-      *out = (T)(u >> 16);
+      out[q] = (T)(u >> 16);
     } else {
-      *out = v;
+      out[q] = v;
     }
   }
 }
 
-hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
-  if (a.head_dim > 128 || n_groups <= 0) return hipErrorInvalidValue;
-  dim3 grid(n_groups, a.n_kv_heads, a.jmax);
-  if (dtype == 1) hipLaunchKernelGGL(attn_kernel<bf16>, grid, dim3(ATT_THREADS), 0, s, a);
-  else hipLaunchKernelGGL(attn_kernel<float>, grid, dim3(ATT_THREADS), 0, s, a);
+template <typename T>
+static hipError_t launch_attn_t(const AttnArgs &a, dim3 grid, hipStream_t s) {
+  switch (a.head_dim) {
+    case 32: hipLaunchKernelGGL((attn_kernel<T, 32>), grid, dim3(ATT_THREADS), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((attn_kernel<T, 64>), grid, dim3(ATT_THREADS), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((attn_kernel<T, 128>), grid, dim3(ATT_THREADS), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_comb_t(const CombineArgs &a, dim3 grid, hipStream_t s) {
+  switch (a.head_dim) {
+    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s) {
-  if (rows <= 0) return hipErrorInvalidValue;
+  if (rows <= 0) return hipSuccess;
+  if (a.jmax > ATT_MAX_SPLITS) return hipErrorInvalidValue;
   dim3 grid(rows, a.n_heads);
-  if (dtype == 1) hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(128), 0, s, a);
-  else hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(128), 0, s, a);
-  return hipGetLastError();
+  return dtype == 1 ? launch_comb_t<bf16>(a, grid, s) : launch_comb_t<float>(a, grid, s);
+}
+
+hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
+  if (n_groups <= 0 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
+  dim3 grid(n_groups, a.n_kv_heads, a.jmax);
+  return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);
 }
 
 }  // namespace dex

@@ -19,16 +19,15 @@ enum Epi {
 
 constexpr int GEMM_WAVES = 8;       // split-K ways inside a workgroup
 constexpr int GEMM_THREADS = GEMM_WAVES * 64;
-constexpr int ATT_SPLIT = 256;      // logical keys per attention split
-constexpr int ATT_TILE = 64;        // keys per LDS tile
-constexpr int ATT_THREADS = 256;
-constexpr int ATT_MAX_PAIRS = 64;   // (row, query head) pairs per attention workgroup
+constexpr int ATT_SPLIT = 64;       // logical keys per attention split (one wave)
+constexpr int ATT_THREADS = 64;
+constexpr int ATT_MAX_PAIRS = 64;   // (row, query head) pairs per attention row group
+constexpr int ATT_MAX_SPLITS = 4096; // longest context: 262144 positions
 
 struct GemmArgs {
-  // Weight segments concatenated along the output dimension (QKV uses three,
-  // SWIGLU uses w0 = gate and w1 = up paired column for column).
-  const void *w0, *w1, *w2;
-  int n0, n1, n2;
+  // Weights in the packed block layout (see PackArgs); nsteps_w k-steps per tile.
+  const void *wp;
+  int nsteps_w;
   int N;          // output columns (SWIGLU: d_ffn)
   int K;
   const void *x;  // activations [M][ldx]
@@ -78,7 +77,7 @@ struct AttnArgs {
   // row groups: consecutive rows of one sequence
   const int *grp_row0, *grp_nrows, *grp_seq;
   const int *row_pos, *row_nc, *row_chain_off, *chain;
-  float *part;                // [R][H][jmax][hd + 2]
+  float *part;                // [R][H][jmax][hd + 2] split partials (o, max, sum)
   int jmax;
   float scale;
 };
@@ -90,6 +89,19 @@ struct CombineArgs {
   void *out;                  // [R][H*hd] (T)
   int ld_out;
 };
+
+// Weight packing.  mode 0: rows in order; 1: QKV, the three segments w0/w1/w2
+// concatenated with each tile holding RoPE partner dimensions (i, i + hd/2)
+// of one head; 2: gate (w0) and up (w1) blocks interleaved per step.
+struct PackArgs {
+  const void *w0, *w1, *w2;
+  int n0, n1, n2;
+  int N, K, mode, head_dim;
+  void *out;
+  int nsteps;     // filled by launch_pack
+};
+size_t packed_bytes(int dtype, int N, int K, int mode);
+hipError_t launch_pack(int dtype, const PackArgs &a, hipStream_t s);
 
 // Launchers (return the HIP status of the launch).
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipStream_t s);
@@ -130,7 +142,7 @@ hipError_t launch_commit(const CommitArgs &a, hipStream_t s);
 
 struct CollapseArgs {
   int n_jobs;
-  const int *job;             // [n_jobs][4]: seq, src entry/slot, dst entry/slot, kind (0 kv only, 1 kv + slot state)
+  const int *job;             // [n_jobs][6]: seq, src entry, dst entry, src slot, dst slot, kind (0 kv only, 1 kv + slot state)
   void *kc, *vc;              // cache base
   int n_layers, batch, n_kv_heads, kv_entries, head_dim;
   int elem_bytes;

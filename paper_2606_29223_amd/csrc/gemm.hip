@@ -109,28 +109,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   const int r16 = lane & 15, grp = lane >> 4;
   const int Mloc = min(16 * MB, a.M - m0);
 
-  // ---- this lane's weight rows
-  const T *wrow[NT];
-  bool wok[NT];
-  {
-    int col;
-    if (EPI == EPI_QKV) col = qkv_col(tile, r16, a.head_dim);
-    else col = tile * 16 + r16;
-    if (EPI == EPI_SWIGLU) {
-      wok[0] = col < a.N;
-      wok[NT - 1] = col < a.N;
-      wrow[0] = (const T *)a.w0 + (size_t)(wok[0] ? col : 0) * a.K;
-      wrow[NT - 1] = (const T *)a.w1 + (size_t)(wok[0] ? col : 0) * a.K;
-    } else {
-      const T *base;
-      int r;
-      if (col < a.n0) { base = (const T *)a.w0; r = col; }
-      else if (col < a.n0 + a.n1) { base = (const T *)a.w1; r = col - a.n0; }
-      else { base = (const T *)a.w2; r = col - a.n0 - a.n1; }
-      wok[0] = col < a.N;
-      wrow[0] = base + (size_t)(wok[0] ? r : 0) * a.K;
-    }
-  }
+  // ---- this lane's weight stream: packed 1 KB blocks, one per (tile, step, t)
+  const char *wbase = (const char *)a.wp + (size_t)tile * a.nsteps_w * NT * 1024 + lane * 16;
   // ---- this lane's activation rows (one per M block)
   const T *xrow[MB];
   bool xok[MB];
@@ -147,7 +127,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int nsteps = (a.K + KSTEP - 1) / KSTEP;
+  const int nsteps = a.nsteps_w;
   F wa[U][NT], xa[U][MB], wb[U][NT], xb[U][MB];
 
   auto load_chunk = [&](int s0, F (&w)[U][NT], F (&x)[U][MB]) {
@@ -157,7 +137,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int k = s * KSTEP + grp * EPB;
       const bool kin = (s < nsteps) && (k < a.K);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) w[u][t].v = load16(wrow[t] + k, kin && wok[t]);
+      for (int t = 0; t < NT; ++t) w[u][t].v = load16(wbase + ((size_t)s * NT + t) * 1024, s < nsteps);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) x[u][mb].v = load16_cached(xrow[mb] + k, kin && xok[mb]);
     }
@@ -318,6 +298,52 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       a.amax[(size_t)(m0 + ml) * a.n_tiles + tile] = make_float2(best, __int_as_float(bi));
     }
   }
+}
+
+// Weight packing: block (tile, step, t) holds, for lane l, the 16 bytes of
+// row col(tile, l % 16) at k = step * KSTEP + (l / 16) * EPB (zeros beyond
+// N or K), so that a wave's load of one MFMA step is one contiguous 1 KB.
+template <typename T>
+__global__ __launch_bounds__(64) void pack_kernel(PackArgs a) {
+  constexpr int EPB = 16 / (int)sizeof(T);
+  constexpr int KSTEP = 4 * EPB;
+  const int NT = a.mode == 2 ? 2 : 1;
+  const size_t blk = blockIdx.x;
+  const int t = (int)(blk % NT);
+  const size_t ts = blk / NT;
+  const int step = (int)(ts % a.nsteps);
+  const int tile = (int)(ts / a.nsteps);
+  const int lane = threadIdx.x, r16 = lane & 15, grp = lane >> 4;
+  const int col = (a.mode == 1) ? qkv_col(tile, r16, a.head_dim) : tile * 16 + r16;
+  const int k = step * KSTEP + grp * EPB;
+  u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
+  if (col < a.N && k < a.K) {
+    const T *base;
+    int r;
+    if (a.mode == 2) { base = (const T *)(t == 0 ? a.w0 : a.w1); r = col; }
+    else if (col < a.n0) { base = (const T *)a.w0; r = col; }
+    else if (col < a.n0 + a.n1) { base = (const T *)a.w1; r = col - a.n0; }
+    else { base = (const T *)a.w2; r = col - a.n0 - a.n1; }
+    v = *(const u32x4_t *)(base + (size_t)r * a.K + k);
+  }
+  *((u32x4_t *)((char *)a.out + blk * 1024) + lane) = v;
+}
+
+size_t packed_bytes(int dtype, int N, int K, int mode) {
+  const int kstep = dtype == 1 ? 32 : 16;
+  const size_t tiles = (N + 15) / 16, steps = (K + kstep - 1) / kstep;
+  return tiles * steps * (mode == 2 ? 2 : 1) * 1024;
+}
+
+hipError_t launch_pack(int dtype, const PackArgs &a, hipStream_t s) {
+  const int kstep = dtype == 1 ? 32 : 16;
+  PackArgs b = a;
+  b.nsteps = (a.K + kstep - 1) / kstep;
+  const size_t blocks = (size_t)((a.N + 15) / 16) * b.nsteps * (a.mode == 2 ? 2 : 1);
+  if (blocks == 0) return hipSuccess;
+  if (dtype == 1) hipLaunchKernelGGL(pack_kernel<bf16>, dim3((unsigned)blocks), dim3(64), 0, s, b);
+  else hipLaunchKernelGGL(pack_kernel<float>, dim3((unsigned)blocks), dim3(64), 0, s, b);
+  return hipGetLastError();
 }
 
 template <typename T, int EPI>

@@ -196,8 +196,11 @@ class Decoder:
         c.decs = int(cfg.get("decs", 1) if decs is None else decs)
         c.batch = self.batch
         c.max_context = int(max_context if max_context is not None else cfg["prompt_len"] + cfg["gen_len"])
-        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        # a dedicated stream (default priority, non-blocking): launches on the
+        # legacy null stream would also order against every other stream
+        self.stream = stream if stream is not None else torch.cuda.Stream()
         c.hip_stream = self.stream.cuda_stream
+        torch.cuda.synchronize()                # weights uploaded on other streams are complete
         self.model_struct, self.config_struct = m, c
         self.max_context = c.max_context
         self.ctx = dex_create(m, c)
