@@ -81,6 +81,10 @@ struct dex_ctx {
   std::vector<std::vector<int>> stage_layers;
   // capacities
   int S, R_max, CH_MAX, E, n_part, jmax;
+  // packed weights (library-owned, see PackArgs)
+  std::vector<void *> p_qkv, p_o, p_gu, p_down;
+  void *p_lm = nullptr;
+  int ns_d = 0, ns_hhd = 0, ns_F = 0;
   // device buffers
   void *kc = nullptr, *vc = nullptr;
   float2 *rope = nullptr;
@@ -270,6 +274,7 @@ struct StageTables {
   const int *seq, *pos, *entry, *bnd, *tok, *nc, *chain_off, *chain, *mask_n, *mask_tok, *cand_idx;
   const int *g_row0, *g_nrows, *g_seq;
   int n_groups;
+  double attn_bytes;    // keys/values a layer's attention reads (algorithmic)
 };
 
 double wbytes(const dex_ctx *ctx, double elems) { return elems * ctx->es; }
@@ -285,8 +290,7 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
     // QKV
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_WQ); a.w1 = LW(ctx, l, DEX_P_WK); a.w2 = LW(ctx, l, DEX_P_WV);
-      a.n0 = H * hd; a.n1 = Hkv * hd; a.n2 = Hkv * hd;
+      a.wp = ctx->p_qkv[l]; a.nsteps_w = ctx->ns_d;
       a.N = (H + 2 * Hkv) * hd; a.K = d;
       a.x = xb; a.ldx = d; a.M = M;
       a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
@@ -306,7 +310,7 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
       a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq;
       a.row_pos = t.pos; a.row_nc = t.nc; a.row_chain_off = t.chain_off; a.chain = t.chain;
       a.part = apart; a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
-      TimedLaunch tl(ctx, 1, 0.0);
+      TimedLaunch tl(ctx, 1, t.attn_bytes);
       HIPCHK(launch_attention(ctx->dtype, a, t.n_groups, st));
     }
     {
@@ -319,7 +323,7 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
     // O projection + residual
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_WO); a.n0 = d; a.N = d; a.K = H * hd;
+      a.wp = ctx->p_o[l]; a.nsteps_w = ctx->ns_hhd; a.N = d; a.K = H * hd;
       a.x = att; a.ldx = H * hd; a.M = M;
       a.h = h; a.ld_h = d; a.alpha = alpha;
       a.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM); a.xb = xb;
@@ -330,8 +334,8 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
     // gate/up + SiLU
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_W_GATE); a.w1 = LW(ctx, l, DEX_P_W_UP);
-      a.n0 = F; a.N = F; a.K = d;
+      a.wp = ctx->p_gu[l]; a.nsteps_w = ctx->ns_d;
+      a.N = F; a.K = d;
       a.x = xb; a.ldx = d; a.M = M;
       a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
       a.act = act; a.ld_act = F;
@@ -342,7 +346,7 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
     {
       const bool last = (l == last_layer);
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_W_DOWN); a.n0 = d; a.N = d; a.K = F;
+      a.wp = ctx->p_down[l]; a.nsteps_w = ctx->ns_F; a.N = d; a.K = F;
       a.x = act; a.ldx = F; a.M = M;
       a.h = h; a.ld_h = d; a.alpha = alpha;
       a.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
@@ -373,7 +377,7 @@ dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h,
   const int n_tiles = (ctx->V + 15) / 16;
   {
     GemmArgs a{};
-    a.w0 = ctx->lm_head; a.n0 = ctx->V; a.N = ctx->V; a.K = ctx->d;
+    a.wp = ctx->p_lm; a.nsteps_w = ctx->ns_d; a.N = ctx->V; a.K = ctx->d;
     a.x = ctx->ex_xb; a.ldx = ctx->d; a.M = M;
     a.part = ctx->ex_part; a.n_part = ctx->n_part; a.inv_d = 1.0f / ctx->d; a.eps = ctx->eps;
     a.mask_n = mask_n; a.mask_tok = mask_tok; a.mask_stride = ctx->N;
@@ -446,6 +450,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   if (c->batch < 1 || c->batch > DEX_MAX_BATCH) return bad("batch out of range");
   if (c->width_cap < 0) return bad("width_cap must be >= 0");
   if (c->max_context < 2) return bad("max_context must be >= 2");
+  if ((c->max_context + ATT_SPLIT - 1) / ATT_SPLIT > ATT_MAX_SPLITS) return bad("max_context too long");
   const int N = c->n_explored;
   long long per_seq = c->width_cap > 0 ? c->width_cap : (N - 1 >= 20 ? (1LL << 20) : (1LL << (N - 1)));
   if (per_seq * c->batch > DEX_MAX_ROWS) return bad("rows per round exceed DEX_MAX_ROWS (lower width_cap or batch)");
@@ -531,6 +536,43 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       g_create_error = std::string("initialisation copy failed: ") + hipGetErrorString(e);
       dex_destroy(ctx);
       return DEX_E_HIP;
+    }
+  }
+  // packed weights: every wave load of the skinny GEMMs reads 1 KB contiguously
+  {
+    const int kstep = ctx->dtype == DEX_BF16 ? 32 : 16;
+    ctx->ns_d = (ctx->d + kstep - 1) / kstep;
+    ctx->ns_hhd = (ctx->H * ctx->hd + kstep - 1) / kstep;
+    ctx->ns_F = (ctx->F + kstep - 1) / kstep;
+    const int H = ctx->H, Hkv = ctx->Hkv, hd = ctx->hd, dd = ctx->d, F = ctx->F;
+    auto pack = [&](void **dst, const void *w0, const void *w1, const void *w2, int n0, int n1, int n2, int N,
+                    int K, int mode) -> dex_status {
+      dex_status s2 = dalloc(ctx, dst, packed_bytes(ctx->dtype, N, K, mode));
+      if (s2 != DEX_OK) return s2;
+      PackArgs pa{};
+      pa.w0 = w0; pa.w1 = w1; pa.w2 = w2; pa.n0 = n0; pa.n1 = n1; pa.n2 = n2;
+      pa.N = N; pa.K = K; pa.mode = mode; pa.head_dim = hd; pa.out = *dst;
+      hipError_t e = launch_pack(ctx->dtype, pa, nullptr);
+      if (e != hipSuccess) { ctx->err = std::string("weight packing failed: ") + hipGetErrorString(e); return DEX_E_HIP; }
+      return DEX_OK;
+    };
+    ctx->p_qkv.assign(ctx->L, nullptr); ctx->p_o.assign(ctx->L, nullptr);
+    ctx->p_gu.assign(ctx->L, nullptr); ctx->p_down.assign(ctx->L, nullptr);
+    dex_status ps = DEX_OK;
+    for (int l = 0; l < ctx->L && ps == DEX_OK; ++l) {
+      ps = pack(&ctx->p_qkv[l], LW(ctx, l, DEX_P_WQ), LW(ctx, l, DEX_P_WK), LW(ctx, l, DEX_P_WV), H * hd, Hkv * hd,
+                Hkv * hd, (H + 2 * Hkv) * hd, dd, 1);
+      if (ps == DEX_OK) ps = pack(&ctx->p_o[l], LW(ctx, l, DEX_P_WO), nullptr, nullptr, dd, 0, 0, dd, H * hd, 0);
+      if (ps == DEX_OK)
+        ps = pack(&ctx->p_gu[l], LW(ctx, l, DEX_P_W_GATE), LW(ctx, l, DEX_P_W_UP), nullptr, F, F, 0, F, dd, 2);
+      if (ps == DEX_OK) ps = pack(&ctx->p_down[l], LW(ctx, l, DEX_P_W_DOWN), nullptr, nullptr, dd, 0, 0, dd, F, 0);
+    }
+    if (ps == DEX_OK) ps = pack(&ctx->p_lm, ctx->lm_head, nullptr, nullptr, ctx->V, 0, 0, ctx->V, dd, 0);
+    if (ps == DEX_OK && hipDeviceSynchronize() != hipSuccess) { ctx->err = "weight packing failed"; ps = DEX_E_HIP; }
+    if (ps != DEX_OK) {
+      g_create_error = ctx->err;
+      dex_destroy(ctx);
+      return ps;
     }
   }
   ctx->seqs.resize(ctx->B);
@@ -633,8 +675,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     const float alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_WQ); a.w1 = LW(ctx, l, DEX_P_WK); a.w2 = LW(ctx, l, DEX_P_WV);
-      a.n0 = H * hd; a.n1 = ctx->Hkv * hd; a.n2 = ctx->Hkv * hd;
+      a.wp = ctx->p_qkv[l]; a.nsteps_w = ctx->ns_d;
       a.N = (H + 2 * ctx->Hkv) * hd; a.K = d; a.x = xb; a.ldx = d; a.M = (int)M;
       a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
       a.out = q; a.ld_out = H * hd;
@@ -660,14 +701,14 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     }
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_WO); a.n0 = d; a.N = d; a.K = H * hd; a.x = att; a.ldx = H * hd; a.M = (int)M;
+      a.wp = ctx->p_o[l]; a.nsteps_w = ctx->ns_hhd; a.N = d; a.K = H * hd; a.x = att; a.ldx = H * hd; a.M = (int)M;
       a.h = h; a.ld_h = d; a.alpha = alpha; a.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM); a.xb = xb;
       a.part_out = part; a.n_part_out = ctx->n_part;
       HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
     }
     {
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_W_GATE); a.w1 = LW(ctx, l, DEX_P_W_UP); a.n0 = ctx->F; a.N = ctx->F; a.K = d;
+      a.wp = ctx->p_gu[l]; a.nsteps_w = ctx->ns_d; a.N = ctx->F; a.K = d;
       a.x = xb; a.ldx = d; a.M = (int)M; a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d;
       a.eps = ctx->eps; a.act = act; a.ld_act = ctx->F;
       HIPCHK(launch_gemm(ctx->dtype, EPI_SWIGLU, a, 1, ctx->stream));
@@ -675,7 +716,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     {
       const bool last = l == ctx->L - 1;
       GemmArgs a{};
-      a.w0 = LW(ctx, l, DEX_P_W_DOWN); a.n0 = d; a.N = d; a.K = ctx->F; a.x = act; a.ldx = ctx->F; a.M = (int)M;
+      a.wp = ctx->p_down[l]; a.nsteps_w = ctx->ns_F; a.N = d; a.K = ctx->F; a.x = act; a.ldx = ctx->F; a.M = (int)M;
       a.h = h; a.ld_h = d; a.alpha = alpha;
       a.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
       a.xb = last ? nullptr : xb; a.part_out = part; a.n_part_out = ctx->n_part;
@@ -832,6 +873,13 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     t.tok = dptr(t_tok) + r0; t.nc = dptr(t_nc) + r0; t.chain_off = dptr(t_coff) + r0; t.chain = dptr(t_chain);
     t.g_row0 = dptr(t_g0) + stage_g0[k]; t.g_nrows = dptr(t_gn) + stage_g0[k]; t.g_seq = dptr(t_gs) + stage_g0[k];
     t.n_groups = stage_g0[k + 1] - stage_g0[k];
+    t.attn_bytes = 0.0;
+    for (int g = stage_g0[k]; g < stage_g0[k + 1]; ++g) {
+      int mp = 0;
+      for (int r = stage_r0[k] + t_g0[g]; r < stage_r0[k] + t_g0[g] + t_gn[g]; ++r) mp = std::max(mp, t_pos[r]);
+      t.attn_bytes += (double)(mp + 1) * 2.0 * ctx->Hkv * ctx->hd * ctx->es;
+    }
+    t.attn_bytes += (double)M * ctx->H * ctx->hd * (4.0 + ctx->es);
     {
       PrepArgs p{};
       p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
@@ -1032,9 +1080,17 @@ dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, co
   if (!W || !x || !y || N < 1 || K < 1 || M < 1 || M > 64) return DEX_E_INVAL;
   if (dtype != DEX_F32 && dtype != DEX_BF16) return DEX_E_INVAL;
   if (K % (dtype == DEX_BF16 ? 8 : 4)) return DEX_E_INVAL;
+  void *wp = nullptr;
+  if (hipMalloc(&wp, packed_bytes(dtype, N, K, 0)) != hipSuccess) return DEX_E_NOMEM;
+  PackArgs pa{};
+  pa.w0 = W; pa.n0 = N; pa.N = N; pa.K = K; pa.mode = 0; pa.head_dim = 16; pa.out = wp;
+  hipError_t e = launch_pack(dtype, pa, (hipStream_t)stream);
   GemmArgs a{};
-  a.w0 = W; a.n0 = N; a.N = N; a.K = K; a.x = x; a.ldx = K; a.M = M; a.out = y; a.ld_out = N;
-  hipError_t e = launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
+  a.wp = wp; a.nsteps_w = (K + (dtype == DEX_BF16 ? 32 : 16) - 1) / (dtype == DEX_BF16 ? 32 : 16);
+  a.N = N; a.K = K; a.x = x; a.ldx = K; a.M = M; a.out = y; a.ld_out = N;
+  if (e == hipSuccess) e = launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  (void)hipFree(wp);
   return e == hipSuccess ? DEX_OK : DEX_E_HIP;
 }
 
