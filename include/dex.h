@@ -187,6 +187,15 @@ dex_status dex_debug_slot_entry(dex_ctx *ctx, int32_t seq, int32_t slot, int32_t
 dex_status dex_debug_set_kernel_timing(dex_ctx *ctx, int32_t enable);
 dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *launches, double *bytes);
 
+/* Mean duration of one decode-step GEMM class (3 o-proj, 4 gate/up, 5 down,
+ * 6 lm-head) at M rows: `reps` back-to-back launches on the context's stream
+ * between two hipEvents, cycling through the layers' weights so that no
+ * launch re-reads a matrix another launch just streamed.  Uses the context's
+ * scratch buffers (the decode state is untouched).  *bytes_per_launch is the
+ * algorithmic traffic of one launch (weights plus activations).            */
+dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t reps, double *avg_us,
+                                 double *bytes_per_launch);
+
 /* Stand-alone skinny GEMM y[M][N] = x[M][K] * W[N][K]^T (float32 out) on the
  * same matrix-core kernel the decode step uses.  dtype: dex_dtype of W and x.
  * Device pointers; M in [1, 64].  For tests of batch invariance.            */

@@ -1075,6 +1075,61 @@ dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *
   return DEX_OK;
 }
 
+dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t reps, double *avg_us,
+                                 double *bytes_per_launch) {
+  if (!ctx || !avg_us || !bytes_per_launch || M < 1 || M > ctx->R_max || reps < 1) return DEX_E_INVAL;
+  if (cls != 3 && cls != 4 && cls != 5 && cls != 6) { ctx->err = "only o-proj, gate/up, down, lm-head"; return DEX_E_INVAL; }
+  if (!ctx->prefilled) { ctx->err = "time_kernel needs a prefilled context"; return DEX_E_STATE; }
+  const int d = ctx->d, H = ctx->H, hd = ctx->hd, F = ctx->F;
+  hipEvent_t e0, e1;
+  HIPCHK(hipEventCreate(&e0));
+  HIPCHK(hipEventCreate(&e1));
+  double bytes = 0.0;
+  auto launch = [&](int rep) -> hipError_t {
+    const int l = rep % ctx->L;
+    GemmArgs a{};
+    a.M = M;
+    int epi = EPI_RESID;
+    if (cls == 3) {
+      a.wp = ctx->p_o[l]; a.nsteps_w = ctx->ns_hhd; a.N = d; a.K = H * hd; a.x = ctx->att_w; a.ldx = H * hd;
+      a.h = ctx->h_w; a.ld_h = d; a.alpha = 0.f; a.part_out = ctx->part_w; a.n_part_out = ctx->n_part;
+      bytes = (double)ctx->es * ((double)d * H * hd + (double)M * H * hd + (double)M * d) + 8.0 * M * d;
+    } else if (cls == 4) {
+      a.wp = ctx->p_gu[l]; a.nsteps_w = ctx->ns_d; a.N = F; a.K = d; a.x = ctx->xb_w; a.ldx = d;
+      a.part = ctx->part_w; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+      a.act = ctx->act_w; a.ld_act = F;
+      epi = EPI_SWIGLU;
+      bytes = (double)ctx->es * (2.0 * F * d + (double)M * d + (double)M * F);
+    } else if (cls == 5) {
+      a.wp = ctx->p_down[l]; a.nsteps_w = ctx->ns_F; a.N = d; a.K = F; a.x = ctx->act_w; a.ldx = F;
+      a.h = ctx->h_w; a.ld_h = d; a.alpha = 0.f; a.part_out = ctx->part_w; a.n_part_out = ctx->n_part;
+      bytes = (double)ctx->es * ((double)d * F + (double)M * F + (double)M * d) + 8.0 * M * d;
+    } else {
+      a.wp = ctx->p_lm; a.nsteps_w = ctx->ns_d; a.N = ctx->V; a.K = d; a.x = ctx->ex_xb; a.ldx = d;
+      a.part = ctx->ex_part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+      a.mask_n = ctx->tab_dev; a.mask_tok = ctx->tab_dev; a.mask_stride = 0;
+      a.amax = ctx->amax; a.n_tiles = (ctx->V + 15) / 16;
+      epi = EPI_LOGITS;
+      bytes = (double)ctx->es * ((double)ctx->V * d + (double)M * d);
+    }
+    return launch_gemm(ctx->dtype, epi, a, 1, ctx->stream);
+  };
+  // zero mask counts for the LM head (the row tables are rewritten every round)
+  if (cls == 6) HIPCHK(hipMemsetAsync(ctx->tab_dev, 0, (size_t)M * 4, ctx->stream));
+  HIPCHK(launch(0));                       // warm the code object
+  HIPCHK(hipEventRecord(e0, ctx->stream));
+  for (int i = 0; i < reps; ++i) HIPCHK(launch(i + 1));
+  HIPCHK(hipEventRecord(e1, ctx->stream));
+  HIPCHK(hipEventSynchronize(e1));
+  float ms = 0.f;
+  HIPCHK(hipEventElapsedTime(&ms, e0, e1));
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  *avg_us = (double)ms * 1e3 / reps;
+  *bytes_per_launch = bytes;
+  return DEX_OK;
+}
+
 dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M, float *y,
                           void *stream) {
   if (!W || !x || !y || N < 1 || K < 1 || M < 1 || M > 64) return DEX_E_INVAL;

@@ -24,7 +24,7 @@ EXPORTED = (
     "dex_create", "dex_prefill", "dex_step", "dex_destroy", "dex_last_error",
     "dex_debug_set_logits_tap", "dex_debug_lattice", "dex_debug_last_collapse",
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
-    "dex_debug_kernel_times", "dex_debug_gemm", "dex_debug_copy",
+    "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_copy",
 )
 
 
@@ -93,6 +93,7 @@ def load(path: str | None = None):
     lib.dex_debug_slot_entry.argtypes = [vp, i32, i32, P(i32)]
     lib.dex_debug_set_kernel_timing.argtypes = [vp, i32]
     lib.dex_debug_kernel_times.argtypes = [vp, i32, P(ctypes.c_double), P(i64), P(ctypes.c_double)]
+    lib.dex_debug_time_kernel.argtypes = [vp, i32, i32, i32, P(ctypes.c_double), P(ctypes.c_double)]
     lib.dex_debug_gemm.argtypes = [i32, vp, i32, i32, vp, i32, vp, vp]
     lib.dex_debug_copy.argtypes = [vp, vp, i64, vp]
     for name in EXPORTED:
@@ -251,6 +252,13 @@ class Decoder:
         b = (ctypes.c_double * 8)()
         _check(self.lib, self.ctx, self.lib.dex_debug_kernel_times(self.ctx, 8, ms, n, b))
         return list(ms), list(n), list(b)
+
+    def time_kernel(self, cls: int, M: int, reps: int = 64):
+        """(mean microseconds, algorithmic bytes) of one decode GEMM launch."""
+        us, b = ctypes.c_double(), ctypes.c_double()
+        _check(self.lib, self.ctx, self.lib.dex_debug_time_kernel(self.ctx, cls, M, reps, ctypes.byref(us),
+                                                                  ctypes.byref(b)))
+        return us.value, b.value
 
     def close(self):
         if self.ctx:

@@ -1,0 +1,164 @@
+"""Turn rocprofv3 CSV output into the short text summaries kept in profiles/.
+
+  python3 -m paper_2606_29223_amd.profile_summary stats STATS.csv TRACE.csv \
+      --command "..." --out profiles/NAME.txt
+  python3 -m paper_2606_29223_amd.profile_summary traffic FETCH_DIR WRITE_DIR \
+      --command "..." --out-json profiles/traffic.json --out profiles/NAME.txt
+
+`stats` lists the kernels by total time and, for the decode GEMMs and the
+attention kernels, the median duration of their decode launches.  `traffic`
+reads the FETCH_SIZE and WRITE_SIZE passes over `traffic_run`, derives the
+scale factor from the plain copy kernel (known bytes read and written) and
+reports bytes per launch for each decode GEMM class next to its algorithmic
+bytes.  The JSON records a hash of the GEMM kernel source so that a later
+change of the kernel invalidates the measurement.
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+SHORT = {
+    "gemm_kernel<unsigned short, 1, 1>": "qkv (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 2, 1>": "o-proj / down (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 3, 1>": "gate/up (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 4, 1>": "lm-head (bf16, M<=16)",
+}
+
+
+def gemm_source_hash() -> str:
+    h = hashlib.sha1()
+    for f in ("gemm.hip", "dex_kernels.h"):
+        h.update(open(os.path.join(PKG, "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def _short(name: str) -> str:
+    base = name.split("(")[0].replace("void ", "").replace("dex::", "")
+    return base
+
+
+def stats(args):
+    rows = list(csv.DictReader(open(args.stats_csv)))
+    trace = list(csv.DictReader(open(args.trace_csv))) if args.trace_csv else []
+    lines = [f"command: {args.command}", "", "rocprofv3 kernel statistics (all dispatches of the run)", ""]
+    lines.append(f"{'kernel':58s} {'calls':>7s} {'avg_us':>9s} {'total_ms':>9s} {'pct':>6s}")
+    for r in rows[: args.top]:
+        lines.append(f"{_short(r['Name'])[:58]:58s} {r['Calls']:>7s} {float(r['AverageNs']) / 1e3:9.2f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:9.2f} {float(r['Percentage']):6.1f}")
+    if trace:
+        lines += ["", "decode launches (median duration; decode = M <= 16 GEMMs, attention grid x <= 256)"]
+        groups = {}
+        for t in trace:
+            n = _short(t["Kernel_Name"])
+            dur = (int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e3
+            key = None
+            for k, v in SHORT.items():
+                if n.startswith(k):
+                    key = v
+            if n.startswith("attn_kernel") and int(t["Grid_Size_X"]) <= 256 * 64:
+                key = "attention (decode)"
+            if n.startswith("combine_kernel") and int(t["Grid_Size_X"]) <= 256 * 64:
+                key = "attention combine (decode)"
+            if key:
+                groups.setdefault(key, []).append(dur)
+        for k in sorted(groups):
+            v = groups[k]
+            lines.append(f"  {k:34s} launches={len(v):6d} median_us={statistics.median(v):8.2f}")
+    os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _counter_rows(d):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = list(csv.DictReader(open(files[0])))
+    rows.sort(key=lambda r: int(r.get("Dispatch_Id", r.get("Correlation_Id", 0))))
+    return rows
+
+
+def _per_dispatch(rows, counter):
+    out = []
+    for r in rows:
+        if r["Counter_Name"] == counter:
+            out.append((_short(r["Kernel_Name"]), float(r["Counter_Value"])))
+    return out
+
+
+def traffic(args):
+    run = json.load(open(args.run_json)) if args.run_json else None
+    reps = args.reps
+    res = {}
+    for counter, d in (("FETCH_SIZE", args.fetch_dir), ("WRITE_SIZE", args.write_dir)):
+        disp = _per_dispatch(_counter_rows(d), counter)
+        copies = [v for n, v in disp if n.startswith("copy_kernel")]
+        res[counter] = {"copy_kib": statistics.median(copies)}
+        # the decode GEMM launches of traffic_run: (reps + 1) per class, in class order
+        seq = {"o_proj": ("gemm_kernel<unsigned short, 2, 1>", 0),
+               "down": ("gemm_kernel<unsigned short, 2, 1>", 1),
+               "gate_up": ("gemm_kernel<unsigned short, 3, 1>", 0),
+               "lm_head": ("gemm_kernel<unsigned short, 4, 1>", 0)}
+        for cls, (name, idx) in seq.items():
+            vals = [v for n, v in disp if n.startswith(name)]
+            groups = {"gemm_kernel<unsigned short, 2, 1>": 2}.get(name, 1)
+            vals = vals[-groups * (reps + 1):]
+            vals = vals[idx * (reps + 1) + 1:(idx + 1) * (reps + 1)]   # drop the warm-up launch
+            res[counter][cls] = statistics.median(vals) if vals else None
+    copy_bytes = 1 << 30
+    f_scale = copy_bytes / (res["FETCH_SIZE"]["copy_kib"] * 1024.0)
+    w_scale = copy_bytes / (res["WRITE_SIZE"]["copy_kib"] * 1024.0)
+    out = {"gemm_source": gemm_source_hash(), "fetch_scale": f_scale, "write_scale": w_scale,
+           "command": args.command, "rows": 1}
+    cfg = args.config
+    out[cfg] = {}
+    lines = [f"command: {args.command}", "",
+             f"calibration: plain copy of {copy_bytes} bytes read FETCH_SIZE={res['FETCH_SIZE']['copy_kib']:.0f} KiB, "
+             f"WRITE_SIZE={res['WRITE_SIZE']['copy_kib']:.0f} KiB -> scale fetch {f_scale:.4f}, write {w_scale:.4f}", "",
+             f"{'kernel':10s} {'fetch_MB':>10s} {'write_MB':>10s} {'traffic_MB':>11s} {'algorithmic_MB':>15s}"]
+    for cls in ("o_proj", "gate_up", "down", "lm_head"):
+        fk, wk = res["FETCH_SIZE"][cls], res["WRITE_SIZE"][cls]
+        if fk is None or wk is None:
+            continue
+        fb, wb = fk * 1024.0 * f_scale, wk * 1024.0 * w_scale
+        alg = run["kernels"][cls]["algorithmic_bytes"] if run else None
+        out[cfg][cls] = {"bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb, "algorithmic_bytes": alg}
+        lines.append(f"{cls:10s} {fb / 1e6:10.2f} {wb / 1e6:10.3f} {(fb + wb) / 1e6:11.2f} "
+                     f"{(alg or 0) / 1e6:15.2f}")
+    json.dump(out, open(args.out_json, "w"), indent=1)
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("stats_csv")
+    s.add_argument("trace_csv", nargs="?")
+    s.add_argument("--command", required=True)
+    s.add_argument("--out", required=True)
+    s.add_argument("--top", type=int, default=16)
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch_dir")
+    t.add_argument("write_dir")
+    t.add_argument("--run-json", default=None)
+    t.add_argument("--reps", type=int, default=8)
+    t.add_argument("--config", default="llama-32L-d4096-x8-w4")
+    t.add_argument("--command", required=True)
+    t.add_argument("--out-json", required=True)
+    t.add_argument("--out", required=True)
+    a = ap.parse_args()
+    stats(a) if a.cmd == "stats" else traffic(a)
+
+
+if __name__ == "__main__":
+    main()
