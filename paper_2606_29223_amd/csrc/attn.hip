@@ -314,4 +314,203 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStrea
   return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);
 }
 
+
+// ------------------------------------------------------------------------
+// Causal prompt attention on the matrix cores (bf16 keys/values).
+//
+// Workgroup = (32 query rows, kv head, sequence); wave w is query head
+// kvh * G + w.  Key blocks of 64 positions are staged in LDS -- K as
+// [key][dim] and V transposed as [dim][key], rows padded so the 16-byte
+// operand reads of a wave hit distinct banks -- and each wave runs
+//   S = Q K^T   (v_mfma_f32_16x16x32_bf16, 2 x 4 tiles of 16 x 16),
+// an online softmax per query row (causal mask on the diagonal block),
+//   O += P V    (P rounded to bf16 through a per-wave LDS tile),
+// and finally writes O / l.  Only prompt prefill uses it: its results feed
+// plain and lattice decoding alike.
+typedef __attribute__((ext_vector_type(8))) __bf16 pf_bf16x8;
+typedef __attribute__((ext_vector_type(4))) float pf_f32x4;
+
+__device__ __forceinline__ uint16_t pf_f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <int HD>
+__global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
+  constexpr int QB = 32, KB = 64;
+  constexpr int KS = HD / 32;          // MFMA k-steps over head dims
+  constexpr int DT = HD / 16;          // 16-wide output tiles over head dims
+  constexpr int KROW = HD + 8;         // bf16 elements per padded K row
+  constexpr int VROW = KB + 8;         // bf16 elements per padded V^T / P row
+  __shared__ __attribute__((aligned(16))) uint16_t ks[KB][KROW];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[HD][VROW];
+  __shared__ __attribute__((aligned(16))) uint16_t pt[8][QB][VROW];
+
+  const int qb = blockIdx.x, kvh = blockIdx.y, seq = blockIdx.z;
+  const int G = a.n_heads / a.n_kv_heads;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nthr = blockDim.x;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int h = kvh * G + wave;
+  const int P = a.prompt_len;
+  const int q0 = qb * QB;
+  const size_t row_base = (size_t)seq * P;
+  const uint16_t *kbase = (const uint16_t *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const uint16_t *vbase = (const uint16_t *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+
+  // Q fragments (A operand): lane holds row r16 of each 16-row tile, dims
+  // ks*32 + grp*8 .. +8, rounded to bf16
+  pf_bf16x8 qf[2][KS];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int row = q0 + mt * 16 + r16;
+    const bool ok = row < P;
+    const float *src = a.q + (row_base + (ok ? row : 0)) * a.ldq + h * HD;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      uint16_t t[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = ok ? pf_f2bf(src[s * 32 + grp * 8 + e]) : (uint16_t)0;
+      uint4 u;
+      u.x = t[0] | ((uint32_t)t[1] << 16); u.y = t[2] | ((uint32_t)t[3] << 16);
+      u.z = t[4] | ((uint32_t)t[5] << 16); u.w = t[6] | ((uint32_t)t[7] << 16);
+      qf[mt][s] = __builtin_bit_cast(pf_bf16x8, u);
+    }
+  }
+  pf_f32x4 o[2][DT];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[mt][dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun[2][4], lrun[2][4];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { mrun[mt][i] = -INFINITY; lrun[mt][i] = 0.f; }
+
+  const int last_row = min(q0 + QB, P) - 1;
+  for (int k0 = 0; k0 <= last_row; k0 += KB) {
+    __syncthreads();
+    // stage K [key][dim] and V^T [dim][key] (zeros past the prompt)
+    for (int e = threadIdx.x; e < KB * (HD / 8); e += nthr) {
+      const int j = e / (HD / 8), c = e % (HD / 8);
+      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      if (k0 + j < P) {
+        kv = *(const uint4 *)(kbase + (size_t)(k0 + j) * HD + c * 8);
+        vv = *(const uint4 *)(vbase + (size_t)(k0 + j) * HD + c * 8);
+      }
+      *(uint4 *)&ks[j][c * 8] = kv;
+      const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        vt[c * 8 + 2 * q][j] = (uint16_t)(w[q] & 0xffffu);
+        vt[c * 8 + 2 * q + 1][j] = (uint16_t)(w[q] >> 16);
+      }
+    }
+    __syncthreads();
+    if (wave < G) {
+      // S = Q K^T
+      pf_f32x4 s[2][4];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) s[mt][nt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const pf_bf16x8 kb = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&ks[nt * 16 + r16][st * 32 + grp * 8]);
+#pragma unroll
+          for (int mt = 0; mt < 2; ++mt)
+            s[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[mt][st], kb, s[mt][nt], 0, 0, 0);
+        }
+      }
+      // online softmax: lane holds rows mt*16 + grp*4 + i, key nt*16 + r16
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = q0 + mt * 16 + grp * 4 + i;
+          float mx = -INFINITY;
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) {
+            const int key = k0 + nt * 16 + r16;
+            float v = s[mt][nt][i] * a.scale;
+            if (key > row || key >= P) v = -INFINITY;
+            s[mt][nt][i] = v;
+            mx = fmaxf(mx, v);
+          }
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+          const float mnew = fmaxf(mrun[mt][i], mx);
+          const float alpha = (mnew == -INFINITY) ? 1.f : expf(mrun[mt][i] - mnew);
+          float sum = 0.f;
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) {
+            const float p = (s[mt][nt][i] == -INFINITY) ? 0.f : expf(s[mt][nt][i] - mnew);
+            s[mt][nt][i] = p;
+            sum += p;
+          }
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+          lrun[mt][i] = lrun[mt][i] * alpha + sum;
+          mrun[mt][i] = mnew;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[mt][dt][i] *= alpha;
+        }
+      }
+      // P (bf16) to this wave's LDS tile, then O += P V
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pt[wave][mt * 16 + grp * 4 + i][nt * 16 + r16] = pf_f2bf(s[mt][nt][i]);
+    }
+    __syncthreads();
+    if (wave < G) {
+#pragma unroll
+      for (int st = 0; st < KB / 32; ++st) {
+        pf_bf16x8 pa[2];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          pa[mt] = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&pt[wave][mt * 16 + r16][st * 32 + grp * 8]);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const pf_bf16x8 vb = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&vt[dt * 16 + r16][st * 32 + grp * 8]);
+#pragma unroll
+          for (int mt = 0; mt < 2; ++mt) o[mt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[mt], vb, o[mt][dt], 0, 0, 0);
+        }
+      }
+    }
+  }
+  if (wave >= G) return;
+  // O / l -> bf16; lane holds rows mt*16 + grp*4 + i, dim dt*16 + r16
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = q0 + mt * 16 + grp * 4 + i;
+      if (row >= P) continue;
+      uint16_t *dst = (uint16_t *)a.out + (row_base + row) * a.ld_out + h * HD;
+      const float inv = 1.f / lrun[mt][i];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = pf_f2bf(o[mt][dt][i] * inv);
+    }
+}
+
+hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
+  const int G = a.n_heads / a.n_kv_heads;
+  if (G < 1 || G > 8 || a.prompt_len < 1) return hipErrorInvalidValue;
+  dim3 grid((a.prompt_len + 31) / 32, a.n_kv_heads, a.batch);
+  dim3 block(64 * G);
+  switch (a.head_dim) {
+    case 64: hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, block, 0, s, a); break;
+    case 128: hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace dex

@@ -90,6 +90,20 @@ struct CombineArgs {
   int ld_out;
 };
 
+// Causal prompt attention on the matrix cores (bf16 keys/values, head_dim 64
+// or 128): rows are (sequence, position) in order, keys are the committed
+// cache entries 0..position.
+struct PrefillAttnArgs {
+  const float *q;             // [batch * prompt_len][ldq], RoPE applied
+  int ldq;
+  const void *kc, *vc;        // this layer's cache base
+  int kv_entries, n_kv_heads, n_heads, head_dim, batch, prompt_len;
+  float scale;
+  void *out;                  // [batch * prompt_len][ld_out] (bf16)
+  int ld_out;
+};
+hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s);
+
 // Weight packing.  mode 0: rows in order; 1: QKV, the three segments w0/w1/w2
 // concatenated with each tile holding RoPE partner dimensions (i, i + hd/2)
 // of one head; 2: gate (w0) and up (w1) blocks interleaved per step.

@@ -590,6 +590,8 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     if (prompts[i] < 0 || prompts[i] >= ctx->V) { ctx->err = "prompt token out of range"; return DEX_E_INVAL; }
   const size_t M = (size_t)B * P, es = ctx->es;
   const int G = H / ctx->Hkv;
+  // matrix-core prompt attention for bf16 caches; the split kernel otherwise
+  const bool mfma_prefill = ctx->dtype == DEX_BF16 && (hd == 64 || hd == 128) && G <= 8;
   const int grp_rows = std::max(1, ATT_MAX_PAIRS / G);
   const int jmax = (P + ATT_SPLIT - 1) / ATT_SPLIT;
   // attention row chunk bounded so its split partials stay below ~512 MiB
@@ -612,7 +614,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
   A((void **)&q, M * H * hd * 4);
   A(&att, M * H * hd * es);
   A(&act, M * ctx->F * es);
-  A((void **)&apart, chunk * per_row);
+  if (!mfma_prefill) A((void **)&apart, chunk * per_row);
   const size_t n_groups_total = (size_t)B * ((P + grp_rows - 1) / grp_rows);
   const size_t tab_ints = M * 8 + n_groups_total * 4 + 4 * B + 64;
   A((void **)&tab, tab_ints * 4);
@@ -684,7 +686,14 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.row_seq = d_seq; a.row_pos = d_pos; a.row_entry = d_entry; a.rope = ctx->rope;
       HIPCHK(launch_gemm(ctx->dtype, EPI_QKV, a, 1, ctx->stream));
     }
-    for (const auto &ch : chunks) {
+    if (mfma_prefill) {
+      PrefillAttnArgs a{};
+      a.q = q; a.ldq = H * hd;
+      a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
+      a.kv_entries = ctx->E; a.n_kv_heads = ctx->Hkv; a.n_heads = H; a.head_dim = hd; a.batch = B;
+      a.prompt_len = P; a.scale = 1.0f / std::sqrt((float)hd); a.out = att; a.ld_out = H * hd;
+      HIPCHK(launch_prefill_attention(a, ctx->stream));
+    } else for (const auto &ch : chunks) {
       const int g_first = ch[0], g_cnt = ch[1], c0 = ch[2], cn = ch[3];
       AttnArgs a{};
       a.q = q + (size_t)c0 * H * hd; a.ldq = H * hd;

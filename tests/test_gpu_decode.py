@@ -18,7 +18,7 @@ import oracle
 from oracle import ar, dex
 from oracle.lattice import Lattice
 from synth import configs, gen
-from tests.gpu_common import (LOGIT_RTOL, check_tokens_teacher_forced, decoder, host_weights,
+from tests.gpu_common import (GAP, LOGIT_RTOL, check_tokens_teacher_forced, decoder, device_weights, host_weights,
                               max_rel_err, torch_cuda)
 
 pytestmark = pytest.mark.gpu
@@ -245,3 +245,41 @@ def test_small_bf16_lossless_and_oracle():
             if slot == 0:
                 worst = max(worst, max_rel_err(rd["logits"][r], z[pos - P, stage]))
     assert worst <= LOGIT_RTOL, worst
+
+
+@pytest.mark.parametrize("P", [1, 45, 97])
+def test_small_bf16_prefill_ragged_prompts(P):
+    """Prompt lengths that are not a multiple of the 32-query / 64-key tiles
+    of the matrix-core prompt attention (and the one-token prompt), at batch
+    2: y_0 and the next tokens follow the float64 oracle (near ties aside) and
+    the exit logits of every decoded row agree within 2e-2 (max relative)."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = configs.get(SMALL, prompt_len=P, batch=2, prompt_seeds=[7001, 7002])
+    _, w = host_weights(SMALL)
+    T = 5
+    dec = dexlib.Decoder(cfg, device_weights(SMALL), explored=[cfg["n_layers"]], width_cap=1,
+                         max_context=P + T)
+    tap = torch.empty((8, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    prompt = gen.prompts(cfg)
+    toks, rounds = _run(dec, prompt, T, tap=tap, collapse=False)
+    dec.close()
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    for b in range(2):
+        pl = [int(t) for t in prompt[b]]
+        seq = [int(t) for t in toks[b]]
+        pf = m.prefill(pl)
+        z0 = m.exit_logits(pf[2])
+        if seq[0] != int(np.argmax(z0)):
+            srt = np.sort(z0)
+            assert srt[-1] - srt[-2] < GAP and z0.max() - z0[seq[0]] < GAP
+        z = ar.depth_logits(m, pl, seq, [cfg["n_layers"]], prefill=pf)
+        check_tokens_teacher_forced(z[:, -1], seq)
+        seen = 0
+        for rd in rounds:
+            for r, (s, slot, stage, pos, tok) in enumerate(rd["rows"]):
+                if s == b and pos - P < len(seq) - 1:
+                    assert max_rel_err(rd["logits"][r], z[pos - P, 0]) <= LOGIT_RTOL
+                    seen += 1
+        assert seen == T - 1
