@@ -196,9 +196,11 @@ dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *
 dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t reps, double *avg_us,
                                  double *bytes_per_launch);
 
-/* Stand-alone skinny GEMM y[M][N] = x[M][K] * W[N][K]^T (float32 out) on the
- * same matrix-core kernel the decode step uses.  dtype: dex_dtype of W and x.
- * Device pointers; M in [1, 64].  For tests of batch invariance.            */
+/* Stand-alone GEMM y[M][N] = x[M][K] * W[N][K]^T (float32 out).  M in
+ * [1, 64] runs the skinny matrix-core kernel the decode step uses (tests of
+ * batch invariance); M > 64 (bf16 only, N a multiple of 16) runs the M-tiled
+ * kernel of the prompt prefill.  dtype: dex_dtype of W and x; K a multiple of
+ * 8 (bf16) or 4 (fp32).  Device pointers.                                   */
 dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M,
                           float *y, void *hip_stream);
 

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdex.so")
 
-SOURCES = ["gemm.hip", "attn.hip", "misc.hip", "engine.cpp"]
+SOURCES = ["gemm.hip", "gemm_prefill.hip", "attn.hip", "misc.hip", "engine.cpp"]
 ARCH = "gfx950"
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"

@@ -6,6 +6,17 @@
 
 namespace dex {
 
+// Output column of local tile row r16 (0..15) of QKV tile `tile`: a tile keeps
+// the two RoPE partners (i, i + hd/2) of one head together -- rows 0..7 are
+// dims 8j..8j+7 and rows 8..15 dims hd/2+8j.. of head tile/(hd/16), j the
+// tile's index inside the head.  Shared by weight packing and the epilogues.
+__device__ __forceinline__ int qkv_col(int tile, int r16, int hd) {
+  const int tph = hd / 16;                 // tiles per head
+  const int head = tile / tph, j = tile % tph;
+  const int dim = (r16 < 8) ? (8 * j + r16) : (hd / 2 + 8 * j + r16 - 8);
+  return head * hd + dim;
+}
+
 typedef uint16_t bf16;
 
 // ---------------------------------------------------------------- epilogues
@@ -119,6 +130,13 @@ hipError_t launch_pack(int dtype, const PackArgs &a, hipStream_t s);
 
 // Launchers (return the HIP status of the launch).
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipStream_t s);
+// Prompt-prefill GEMM (bf16, M-tiled: 128 weight rows x 128 input rows per
+// workgroup) with the QKV / RESID / SWIGLU / PLAIN epilogues.  Requires N a
+// multiple of 16, K a multiple of 8, 16-byte aligned rows and no boundary
+// rows (gemm_tiled_supported); launch_gemm_tiled returns hipErrorInvalidValue
+// otherwise.
+bool gemm_tiled_supported(int epi, const GemmArgs &a);
+hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s);
 hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s);
 hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s);
 

@@ -673,6 +673,11 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
   }
   const size_t layer_kv = (size_t)B * ctx->Hkv * ctx->E * hd * es;
+  // many prompt rows: the M-tiled kernel (bf16); the decode kernel otherwise
+  auto prefill_gemm = [&](int epi, const GemmArgs &a) -> hipError_t {
+    if (ctx->dtype == DEX_BF16 && a.M > 64 && gemm_tiled_supported(epi, a)) return launch_gemm_tiled(epi, a, ctx->stream);
+    return launch_gemm(ctx->dtype, epi, a, 1, ctx->stream);
+  };
   for (int l = 0; l < ctx->L; ++l) {
     const float alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
     {
@@ -684,7 +689,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
       a.kv_entries = ctx->E; a.n_heads = H; a.n_kv_heads = ctx->Hkv; a.head_dim = hd;
       a.row_seq = d_seq; a.row_pos = d_pos; a.row_entry = d_entry; a.rope = ctx->rope;
-      HIPCHK(launch_gemm(ctx->dtype, EPI_QKV, a, 1, ctx->stream));
+      HIPCHK(prefill_gemm(EPI_QKV, a));
     }
     if (mfma_prefill) {
       PrefillAttnArgs a{};
@@ -713,14 +718,14 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.wp = ctx->p_o[l]; a.nsteps_w = ctx->ns_hhd; a.N = d; a.K = H * hd; a.x = att; a.ldx = H * hd; a.M = (int)M;
       a.h = h; a.ld_h = d; a.alpha = alpha; a.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM); a.xb = xb;
       a.part_out = part; a.n_part_out = ctx->n_part;
-      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
+      HIPCHK(prefill_gemm(EPI_RESID, a));
     }
     {
       GemmArgs a{};
       a.wp = ctx->p_gu[l]; a.nsteps_w = ctx->ns_d; a.N = ctx->F; a.K = d;
       a.x = xb; a.ldx = d; a.M = (int)M; a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d;
       a.eps = ctx->eps; a.act = act; a.ld_act = ctx->F;
-      HIPCHK(launch_gemm(ctx->dtype, EPI_SWIGLU, a, 1, ctx->stream));
+      HIPCHK(prefill_gemm(EPI_SWIGLU, a));
     }
     {
       const bool last = l == ctx->L - 1;
@@ -729,7 +734,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.h = h; a.ld_h = d; a.alpha = alpha;
       a.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
       a.xb = last ? nullptr : xb; a.part_out = part; a.n_part_out = ctx->n_part;
-      HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
+      HIPCHK(prefill_gemm(EPI_RESID, a));
     }
   }
   // y_0: final-depth exit head at the last prompt position of every sequence
@@ -1141,8 +1146,9 @@ dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t r
 
 dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M, float *y,
                           void *stream) {
-  if (!W || !x || !y || N < 1 || K < 1 || M < 1 || M > 64) return DEX_E_INVAL;
+  if (!W || !x || !y || N < 1 || K < 1 || M < 1) return DEX_E_INVAL;
   if (dtype != DEX_F32 && dtype != DEX_BF16) return DEX_E_INVAL;
+  if (M > 64 && (dtype != DEX_BF16 || N % 16)) return DEX_E_INVAL;
   if (K % (dtype == DEX_BF16 ? 8 : 4)) return DEX_E_INVAL;
   void *wp = nullptr;
   if (hipMalloc(&wp, packed_bytes(dtype, N, K, 0)) != hipSuccess) return DEX_E_NOMEM;
@@ -1152,7 +1158,8 @@ dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, co
   GemmArgs a{};
   a.wp = wp; a.nsteps_w = (K + (dtype == DEX_BF16 ? 32 : 16) - 1) / (dtype == DEX_BF16 ? 32 : 16);
   a.N = N; a.K = K; a.x = x; a.ldx = K; a.M = M; a.out = y; a.ld_out = N;
-  if (e == hipSuccess) e = launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
+  if (e == hipSuccess)
+    e = M > 64 ? launch_gemm_tiled(EPI_PLAIN, a, (hipStream_t)stream) : launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
   if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
   (void)hipFree(wp);
   return e == hipSuccess ? DEX_OK : DEX_E_HIP;

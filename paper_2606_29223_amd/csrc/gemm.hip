@@ -83,15 +83,6 @@ __device__ __forceinline__ float row_rscale(const float *part, int n_part, float
   return 1.0f / sqrtf(s * inv_d + eps);
 }
 
-// Output column of local tile row r16 (0..15) for tile `tile`.  QKV tiles keep
-// the two RoPE partners (i, i + hd/2) of a head inside one tile.
-__device__ __forceinline__ int qkv_col(int tile, int r16, int hd) {
-  const int tph = hd / 16;                 // tiles per head
-  const int head = tile / tph, j = tile % tph;
-  const int dim = (r16 < 8) ? (8 * j + r16) : (hd / 2 + 8 * j + r16 - 8);
-  return head * hd + dim;
-}
-
 template <typename T, int EPI, int MB>
 __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   using F = Frag<T>;

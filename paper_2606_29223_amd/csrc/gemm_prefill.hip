@@ -1,0 +1,240 @@
+// M-tiled matrix-core GEMM for the prompt prefill on gfx950 (bf16).
+//
+//   acc[m][n] = sum_k x[m][k] * W[n][k]
+//
+// With M = batch x prompt length in the tens of thousands the skinny decode
+// kernel would re-read the activations once per 16-column weight tile; here a
+// workgroup of four waves owns 128 weight rows x 128 input rows and each wave
+// a 64 x 64 block of 4 x 4 v_mfma_f32_16x16x32_bf16 tiles (the gate/up pair:
+// 2 tile pairs x 4).  Both operands come straight from memory in fragment
+// order: the packed weight layout stores one MFMA A fragment of a 16-row tile
+// per 1 KB block, and an input fragment is 16 rows x 64 contiguous bytes.
+// Neighbouring waves share operands through L1/L2.  The next k-step is loaded
+// while the current one is multiplied.
+//
+// The epilogues are those of the decode kernel (RMSNorm row scale, RoPE and
+// the key/value cache write; residual add with the next norm's input and its
+// sum-of-squares partials; SwiGLU), applied to the accumulators in registers:
+// lane (g, r) of a tile holds output rows 4g..4g+3 of input row r, so every
+// store covers four consecutive columns.
+#include "dex_kernels.h"
+
+namespace dex {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 tb_bf16x8;
+typedef __attribute__((ext_vector_type(4))) float tb_f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int tb_u32x4;
+
+constexpr int TB_THREADS = 256;   // 2 x 2 waves
+constexpr int TB_MF = 4;          // 16-row input fragments per wave (64 rows)
+constexpr int TB_ROWS = 128;      // input rows per workgroup
+
+__device__ __forceinline__ uint32_t tb_f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint2 tb_pack4(float a, float b, float c, float d) {
+  return make_uint2(tb_f2bf(a) | (tb_f2bf(b) << 16), tb_f2bf(c) | (tb_f2bf(d) << 16));
+}
+
+template <int EPI>
+__global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
+  constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;   // interleaved gate/up blocks
+  constexpr int TN = 4 / NT;                        // weight tiles per wave
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int n_tiles = a.N / 16;
+  const int tile0 = (blockIdx.x * 2 + (wave & 1)) * TN;
+  const int m_base = blockIdx.y * TB_ROWS + (wave >> 1) * 64;
+  const int nsteps = a.nsteps_w;
+
+  const char *wp[TN];
+  bool tok[TN];
+#pragma unroll
+  for (int t = 0; t < TN; ++t) {
+    tok[t] = tile0 + t < n_tiles;
+    wp[t] = (const char *)a.wp + (size_t)(tok[t] ? tile0 + t : 0) * nsteps * NT * 1024 + lane * 16;
+  }
+  const uint16_t *xr[TB_MF];
+  bool xok[TB_MF];
+#pragma unroll
+  for (int f = 0; f < TB_MF; ++f) {
+    const int m = m_base + f * 16 + r16;
+    xok[f] = m < a.M;
+    xr[f] = (const uint16_t *)a.x + (size_t)(xok[f] ? m : 0) * a.ldx + grp * 8;
+  }
+
+  tb_f32x4 acc[TN][NT][TB_MF];
+#pragma unroll
+  for (int t = 0; t < TN; ++t)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int f = 0; f < TB_MF; ++f) acc[t][nt][f] = tb_f32x4{0.f, 0.f, 0.f, 0.f};
+
+  tb_u32x4 wa[TN][NT], xa[TB_MF], wb[TN][NT], xb[TB_MF];
+  auto load = [&](int s, tb_u32x4 (&w)[TN][NT], tb_u32x4 (&x)[TB_MF]) {
+    const bool sin = s < nsteps;
+    const bool kin = sin && (s * 32 + grp * 8 < a.K);
+#pragma unroll
+    for (int t = 0; t < TN; ++t)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        w[t][nt] = (sin && tok[t]) ? *(const tb_u32x4 *)(wp[t] + ((size_t)s * NT + nt) * 1024)
+                                   : tb_u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int f = 0; f < TB_MF; ++f)
+      x[f] = (kin && xok[f]) ? *(const tb_u32x4 *)(xr[f] + s * 32) : tb_u32x4{0u, 0u, 0u, 0u};
+  };
+  auto mma = [&](const tb_u32x4 (&w)[TN][NT], const tb_u32x4 (&x)[TB_MF]) {
+#pragma unroll
+    for (int t = 0; t < TN; ++t)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int f = 0; f < TB_MF; ++f)
+          acc[t][nt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(tb_bf16x8, w[t][nt]), __builtin_bit_cast(tb_bf16x8, x[f]), acc[t][nt][f], 0, 0, 0);
+  };
+  load(0, wa, xa);
+  for (int s = 0; s < nsteps; s += 2) {
+    load(s + 1, wb, xb);
+    mma(wa, xa);
+    if (s + 1 >= nsteps) break;
+    load(s + 2, wa, xa);
+    mma(wb, xb);
+  }
+
+  // RMSNorm scale of each input row (lane j sums the partials of row
+  // m_base + j in order), then handed to the lanes holding that row
+  float rsc[TB_MF];
+  if (a.part != nullptr) {
+    const int m = m_base + lane;
+    float ss = 0.f;
+    if (m < a.M) {
+      const float *p = a.part + (size_t)m * a.n_part;
+      for (int t = 0; t < a.n_part; ++t) ss += p[t];
+    }
+    const float r = 1.0f / sqrtf(ss * a.inv_d + a.eps);
+#pragma unroll
+    for (int f = 0; f < TB_MF; ++f) rsc[f] = __shfl(r, f * 16 + r16, 64);
+  } else {
+#pragma unroll
+    for (int f = 0; f < TB_MF; ++f) rsc[f] = 1.f;
+  }
+
+#pragma unroll
+  for (int t = 0; t < TN; ++t) {
+    if (!tok[t]) continue;                    // uniform across the wave
+    const int tile = tile0 + t;
+#pragma unroll
+    for (int f = 0; f < TB_MF; ++f) {
+      const int m = m_base + f * 16 + r16;
+      const bool ok = m < a.M;
+      if constexpr (EPI == EPI_PLAIN) {
+        if (ok) {
+          float *o = a.out + (size_t)m * a.ld_out + tile * 16 + grp * 4;
+          *(float4 *)o = make_float4(acc[t][0][f][0], acc[t][0][f][1], acc[t][0][f][2], acc[t][0][f][3]);
+        }
+      } else if constexpr (EPI == EPI_QKV) {
+        const int hd = a.head_dim;
+        const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
+        const int col0 = qkv_col(tile, 0, hd);
+        const int head_col = col0 - col0 % hd;   // first column of this head
+        const int j = tile % (hd / 16);
+        const bool lo = grp < 2;                 // rows 0..7: dims i; rows 8..15: dims i + hd/2
+        const int i0 = 8 * j + (grp & 1) * 4;    // RoPE pair index of this lane's first row
+        float y[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v = acc[t][0][f][i] * rsc[f];
+          const float partner = __shfl_xor(v, 32, 64);
+          y[i] = v;
+          if (ok && head_col < nq + nk) {        // q or k: rotate the pair
+            const float2 cs = a.rope[(size_t)a.row_pos[m] * (hd / 2) + i0 + i];
+            y[i] = lo ? v * cs.x - partner * cs.y : v * cs.x + partner * cs.y;
+          }
+        }
+        if (ok) {
+          const int dim0 = (lo ? 0 : hd / 2) + i0;
+          if (head_col < nq) {
+            *(float4 *)(a.out + (size_t)m * a.ld_out + head_col + dim0) = make_float4(y[0], y[1], y[2], y[3]);
+          } else {
+            const bool isk = head_col < nq + nk;
+            const int g = (isk ? head_col - nq : head_col - nq - nk) / hd;
+            uint16_t *cache = (uint16_t *)(isk ? a.kc : a.vc);
+            const size_t base = (((size_t)a.row_seq[m] * a.n_kv_heads + g) * a.kv_entries + a.row_entry[m]) * hd;
+            *(uint2 *)(cache + base + dim0) = tb_pack4(y[0], y[1], y[2], y[3]);
+          }
+        }
+      } else if constexpr (EPI == EPI_RESID) {
+        const int n0 = tile * 16 + grp * 4;
+        float hn[4] = {0.f, 0.f, 0.f, 0.f};
+        if (ok) {
+          float *hp = a.h + (size_t)m * a.ld_h + n0;
+          const float4 hv = *(const float4 *)hp;
+          hn[0] = hv.x + a.alpha * acc[t][0][f][0];
+          hn[1] = hv.y + a.alpha * acc[t][0][f][1];
+          hn[2] = hv.z + a.alpha * acc[t][0][f][2];
+          hn[3] = hv.w + a.alpha * acc[t][0][f][3];
+          *(float4 *)hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
+          if (a.xb != nullptr) {
+            const float *gn = a.g_next + n0;
+            *(uint2 *)((uint16_t *)a.xb + (size_t)m * a.ld_h + n0) =
+                tb_pack4(gn[0] * hn[0], gn[1] * hn[1], gn[2] * hn[2], gn[3] * hn[3]);
+          }
+        }
+        // sum of squares over the tile's 16 columns: four per lane, then
+        // across the four lane groups that hold the same input row
+        float sq = hn[0] * hn[0] + hn[1] * hn[1] + hn[2] * hn[2] + hn[3] * hn[3];
+        sq += __shfl_xor(sq, 16, 64);
+        sq += __shfl_xor(sq, 32, 64);
+        if (ok && grp == 0) a.part_out[(size_t)m * a.n_part_out + tile] = sq;
+      } else if constexpr (EPI == EPI_SWIGLU) {
+        if (ok) {
+          float o[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float gt = acc[t][0][f][i] * rsc[f], up = acc[t][NT - 1][f][i] * rsc[f];
+            o[i] = gt / (1.0f + expf(-gt)) * up;
+          }
+          *(uint2 *)((uint16_t *)a.act + (size_t)m * a.ld_act + tile * 16 + grp * 4) = tb_pack4(o[0], o[1], o[2], o[3]);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+bool gemm_tiled_supported(int epi, const GemmArgs &a) {
+  if (a.M < 1 || a.N < 16 || a.N % 16 || a.K < 8 || a.K % 8 || a.ldx % 8 || a.row_bnd != nullptr) return false;
+  if ((a.M + TB_ROWS - 1) / TB_ROWS > 65535) return false;
+  switch (epi) {
+    case EPI_PLAIN: return a.ld_out % 4 == 0;
+    case EPI_QKV: return a.ld_out % 4 == 0 && a.head_dim % 16 == 0;
+    case EPI_RESID: return a.ld_h % 4 == 0;
+    case EPI_SWIGLU: return a.ld_act % 4 == 0;
+    default: return false;
+  }
+}
+
+hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s) {
+  if (!gemm_tiled_supported(epi, a)) return hipErrorInvalidValue;
+  const int n_tiles = a.N / 16;
+  const int tiles_per_wg = epi == EPI_SWIGLU ? 4 : 8;
+  dim3 grid((n_tiles + tiles_per_wg - 1) / tiles_per_wg, (a.M + TB_ROWS - 1) / TB_ROWS);
+  dim3 block(TB_THREADS);
+  switch (epi) {
+    case EPI_PLAIN: hipLaunchKernelGGL(gemm_tiled_kernel<EPI_PLAIN>, grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL(gemm_tiled_kernel<EPI_QKV>, grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL(gemm_tiled_kernel<EPI_RESID>, grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL(gemm_tiled_kernel<EPI_SWIGLU>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dex

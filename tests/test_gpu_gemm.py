@@ -1,4 +1,5 @@
-"""GPU: the skinny-M matrix-core GEMM through the C ABI (dex_debug_gemm).
+"""GPU: the matrix-core GEMMs through the C ABI (dex_debug_gemm): the
+skinny-M decode kernel (M <= 64) and the M-tiled prompt kernel (M > 64).
 
 Parity with a float64 reference of the same bf16/fp32 inputs, batch
 invariance (a row's bits do not depend on M or on the other rows), and
@@ -52,6 +53,20 @@ def test_gemm_matches_float64(dtype, N, K):
         err = np.abs(y - ref).max()
         scale = np.sqrt(K) * 0.05
         assert err <= 2e-5 * scale + 1e-6, (M, err)
+
+
+@pytest.mark.parametrize("N,K,M", [(784, 768, 65), (2048, 4096, 300), (96, 14336, 129), (6144, 4096, 1000)])
+def test_tiled_prefill_gemm_matches_float64(N, K, M):
+    """The M-tiled prompt GEMM (M > 64): ragged M against the 128-row
+    workgroup tile, tile counts that leave a workgroup partly idle, long K."""
+    torch = torch_cuda()
+    Wt, xt, W64, x64 = _inputs(torch, 1, N, K, M, 300 + N + M)
+    y = _gemm(torch, 1, Wt, xt, M)
+    ref = x64 @ W64.T
+    err = np.abs(y - ref).max()
+    assert err <= 2e-5 * np.sqrt(K) * 0.05 + 1e-6, err
+    # deterministic run to run
+    assert np.array_equal(y.view(np.uint32), _gemm(torch, 1, Wt, xt, M).view(np.uint32))
 
 
 @pytest.mark.parametrize("dtype", [1, 0])
