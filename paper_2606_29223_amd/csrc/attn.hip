@@ -8,11 +8,11 @@
 // reads key/value head h / (H / Hkv).
 //
 // Work split: one wave per (row group, kv head, split of 64 logical keys).
-// A row group is consecutive rows of one sequence.  Lane i holds the
-// committed key at position s0 + i in registers (loaded once, shared by every
-// row and query head of the group) and the split's committed values are
-// staged in LDS; a row whose logical key at that position lives in a lattice
-// slot reads it from its chain instead.  Per row: the G query heads' scores
+// A row group is consecutive rows of one sequence.  The split's committed
+// keys and values are loaded once with contiguous 1 KB loads and staged in
+// LDS (shared by every row and query head of the group); lane i scores the
+// key at position s0 + i from its LDS row, and a row whose logical key at
+// that position lives in a lattice slot reads it from its chain instead.  Per row: the G query heads' scores
 // run as independent FMA chains over the head dimensions, softmax statistics
 // are wave reductions, and lane i accumulates value dimensions
 // [i*hd/64, (i+1)*hd/64) over the split's keys in position order.  Each split
@@ -79,26 +79,42 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   const T *kbase = (const T *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
   const T *vbase = (const T *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
 
-  // this lane's key lives in its own LDS row: the committed one at position t
-  // (shared by the rows of the group) or a row's chain entry; `held` names
-  // which one is there
+  // committed keys and values of the split, loaded together with the first
+  // row's queries: each instruction covers four whole key rows (1 KB
+  // contiguous), then K goes to one padded LDS row per key (lane i's key
+  // row i) and V to the value tile.  Positions past the committed prefix
+  // stay zero until a row's chain entries are patched in.
   const int t = s0 + lane;
   uint4 *krow = (uint4 *)&ks[lane][0];
-  int held = -1;
-  // committed values of the split in LDS; the rest zero until a row's chain
-  // entries are patched in
   const int tn = max(0, min(ATT_SPLIT, ncmax - s0));
+  // `held` names the key in this lane's LDS row: -2 the committed one at
+  // position t, -1 none, else a cache entry of a row's chain
+  int held = t - s0 < tn ? -2 : -1;
+  constexpr int Q4 = GMAX * HD / 4 / ATT_THREADS;
+  float4 qv[Q4];
+  auto load_q = [&](int r) {
+    const float4 *qsrc = (const float4 *)(a.q + (size_t)r * a.ldq + kvh * G * HD);
+#pragma unroll
+    for (int i = 0; i < Q4; ++i) {
+      const int e = lane + i * ATT_THREADS;
+      qv[i] = (e < G * HD / 4) ? qsrc[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
   {
     constexpr int PER = ATT_SPLIT * V4 / ATT_THREADS;   // 16-byte loads per lane
-    uint4 v[PER];
+    uint4 v[PER], k[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = lane + i * ATT_THREADS, j = e / V4, c = e % V4;
-      v[i] = (j < tn) ? ((const uint4 *)(vbase + (size_t)(s0 + j) * HD))[c] : make_uint4(0, 0, 0, 0);
+      const bool ok = j < tn;
+      k[i] = ok ? ((const uint4 *)(kbase + (size_t)(s0 + j) * HD))[c] : make_uint4(0, 0, 0, 0);
+      v[i] = ok ? ((const uint4 *)(vbase + (size_t)(s0 + j) * HD))[c] : make_uint4(0, 0, 0, 0);
     }
+    load_q(r0);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = lane + i * ATT_THREADS;
+      *((uint4 *)&ks[e / V4][0] + e % V4) = k[i];
       *((uint4 *)&vs[e / V4][0] + e % V4) = v[i];
     }
   }
@@ -107,17 +123,10 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
     const int r = r0 + rr;
     const int pos = a.row_pos[r], nc = a.row_nc[r], coff = a.row_chain_off[r];
     if (s0 > pos) continue;
+    if (rr > 0) load_q(r);
     __syncthreads();
     {
-      const float4 *qsrc = (const float4 *)(a.q + (size_t)r * a.ldq + kvh * G * HD);
       float4 *qdst = (float4 *)&qs[0][0];
-      constexpr int Q4 = GMAX * HD / 4 / ATT_THREADS;
-      float4 qv[Q4];
-#pragma unroll
-      for (int i = 0; i < Q4; ++i) {
-        const int e = lane + i * ATT_THREADS;
-        qv[i] = (e < G * HD / 4) ? qsrc[e] : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
 #pragma unroll
       for (int i = 0; i < Q4; ++i) qdst[lane + i * ATT_THREADS] = qv[i];
     }
@@ -154,11 +163,11 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
           const float4 *q4 = (const float4 *)&qs[g][c * EPC];
 #pragma unroll
           for (int e4 = 0; e4 < EPC / 4; ++e4) {
-            const float4 qv = q4[e4];
-            sacc[g] = fmaf(qv.x, kv[4 * e4 + 0], sacc[g]);
-            sacc[g] = fmaf(qv.y, kv[4 * e4 + 1], sacc[g]);
-            sacc[g] = fmaf(qv.z, kv[4 * e4 + 2], sacc[g]);
-            sacc[g] = fmaf(qv.w, kv[4 * e4 + 3], sacc[g]);
+            const float4 qq = q4[e4];
+            sacc[g] = fmaf(qq.x, kv[4 * e4 + 0], sacc[g]);
+            sacc[g] = fmaf(qq.y, kv[4 * e4 + 1], sacc[g]);
+            sacc[g] = fmaf(qq.z, kv[4 * e4 + 2], sacc[g]);
+            sacc[g] = fmaf(qq.w, kv[4 * e4 + 3], sacc[g]);
           }
         }
       }
@@ -308,11 +317,6 @@ hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t
   return dtype == 1 ? launch_comb_t<bf16>(a, grid, s) : launch_comb_t<float>(a, grid, s);
 }
 
-hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
-  if (n_groups <= 0 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
-  dim3 grid(n_groups, a.n_kv_heads, a.jmax);
-  return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);
-}
 
 
 // ------------------------------------------------------------------------
@@ -500,6 +504,211 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
     }
 }
 
+// ------------------------------------------------------------------------
+// Decode attention on the matrix cores (bf16 caches, head_dim 64 or 128).
+//
+// Same work split and partials as attn_kernel -- one wave per (row group, kv
+// head, split of 64 logical keys), (o, max, sum) per (row, query head,
+// split) -- with the two products on v_mfma_f32_16x16x32_bf16:
+//   S = Q K^T    the (row, query head) pairs of a pass as 16-row tiles, q
+//                rounded to bf16; four 16-key tiles of the split;
+//   O = P V      P = exp(S - max) rounded to bf16 through an LDS tile, V
+//                transposed into LDS ([dim][key]) once per split.
+// Each output element of an MFMA depends only on its own pair's row and its
+// key (or dimension) column, and the softmax statistics reduce over the
+// split's keys in a fixed lane order, so a pair gets the same bits whichever
+// pairs share its tile.  Keys whose position lies in a row's lattice chain
+// are patched into the operands for that row alone: a split holding such
+// keys runs one pass per row, any other split one pass over all its rows.
+// Splits are dispatched last-to-first so that the chain splits, which carry
+// the most passes, start first.
+template <int HD>
+__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
+  constexpr int KS = HD / 32;                 // k-steps of S over head dims
+  constexpr int DT = HD / 16;                 // 16-dim tiles of O
+  constexpr int NKT = ATT_SPLIT / 16;         // 16-key tiles per split
+  constexpr int V4 = HD / 8;                  // 16-byte chunks per key row
+  constexpr int VROW = ATT_SPLIT + 8;         // padded V^T / P row (bf16)
+  __shared__ __attribute__((aligned(16))) uint16_t vt[HD][VROW];
+  __shared__ __attribute__((aligned(16))) uint16_t pt[16][VROW];
+  __shared__ int prow[ATT_MAX_PAIRS];         // group-relative rows of a pass
+
+  const int gi = blockIdx.x, kvh = blockIdx.y;
+  const int split = a.jmax - 1 - (int)blockIdx.z;
+  const int lane = threadIdx.x, r16 = lane & 15, grp = lane >> 4;
+  const int r0 = a.grp_row0[gi], nr = a.grp_nrows[gi], seq = a.grp_seq[gi];
+  const int G = a.n_heads / a.n_kv_heads;
+  const int s0 = split * ATT_SPLIT;
+  int maxpos = -1, ncmax = 0;
+  bool any_chain = false;
+  for (int r = 0; r < nr; ++r) {
+    const int pos = a.row_pos[r0 + r], nc = a.row_nc[r0 + r];
+    maxpos = max(maxpos, pos);
+    ncmax = max(ncmax, nc);
+    any_chain |= max(nc, s0) <= min(pos, s0 + ATT_SPLIT - 1);
+  }
+  if (s0 > maxpos) return;
+  const uint16_t *kbase = (const uint16_t *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const uint16_t *vbase = (const uint16_t *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const int tn = max(0, min(ATT_SPLIT, ncmax - s0));   // committed keys in the split
+
+  // K as B fragments in registers: kf[nt][st] = key s0 + 16 nt + r16, dims
+  // 32 st + 8 grp .. +8
+  uint4 kf[NKT][KS];
+#pragma unroll
+  for (int nt = 0; nt < NKT; ++nt)
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+      const int j = nt * 16 + r16;
+      kf[nt][st] = j < tn ? *(const uint4 *)(kbase + (size_t)(s0 + j) * HD + st * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+    }
+  // V: lane j loads key j's row, then writes it as column j of V^T
+  {
+    uint4 vv[V4];
+#pragma unroll
+    for (int c = 0; c < V4; ++c)
+      vv[c] = lane < tn ? *(const uint4 *)(vbase + (size_t)(s0 + lane) * HD + c * 8) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < V4; ++c) {
+      const uint32_t w[4] = {vv[c].x, vv[c].y, vv[c].z, vv[c].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        vt[c * 8 + 2 * q][lane] = (uint16_t)(w[q] & 0xffffu);
+        vt[c * 8 + 2 * q + 1][lane] = (uint16_t)(w[q] >> 16);
+      }
+    }
+  }
+
+  auto pass = [&](int nrp) {
+    const int P = nrp * G;
+    for (int mt = 0; mt * 16 < P; ++mt) {
+      // A fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
+      const int pa = mt * 16 + r16;
+      const bool pok = pa < P;
+      const int prr = pok ? prow[pa / G] : 0;
+      const float *qsrc = a.q + (size_t)(r0 + prr) * a.ldq + (kvh * G + (pok ? pa % G : 0)) * HD + grp * 8;
+      pf_bf16x8 qf[KS];
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+        if (pok) {
+          x0 = *(const float4 *)(qsrc + st * 32);
+          x1 = *(const float4 *)(qsrc + st * 32 + 4);
+        }
+        uint4 u;
+        u.x = pf_f2bf(x0.x) | ((uint32_t)pf_f2bf(x0.y) << 16);
+        u.y = pf_f2bf(x0.z) | ((uint32_t)pf_f2bf(x0.w) << 16);
+        u.z = pf_f2bf(x1.x) | ((uint32_t)pf_f2bf(x1.y) << 16);
+        u.w = pf_f2bf(x1.z) | ((uint32_t)pf_f2bf(x1.w) << 16);
+        qf[st] = __builtin_bit_cast(pf_bf16x8, u);
+      }
+      pf_f32x4 sc[NKT];
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt) sc[nt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+#pragma unroll
+        for (int nt = 0; nt < NKT; ++nt)
+          sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st], __builtin_bit_cast(pf_bf16x8, kf[nt][st]), sc[nt], 0, 0, 0);
+      // softmax over the split per pair: lane holds pairs mt*16 + 4 grp + i,
+      // keys 16 nt + r16
+      float mrow[4], lrow[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int pc = mt * 16 + grp * 4 + i;
+        const int pos = pc < P ? a.row_pos[r0 + prow[pc / G]] : -1;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int nt = 0; nt < NKT; ++nt) {
+          float v = sc[nt][i] * a.scale;
+          if (s0 + nt * 16 + r16 > pos) v = -INFINITY;
+          sc[nt][i] = v;
+          mx = fmaxf(mx, v);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        float sum = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < NKT; ++nt) {
+          const float e = (mx == -INFINITY) ? 0.f : expf(sc[nt][i] - mx);
+          sum += e;
+          pt[grp * 4 + i][nt * 16 + r16] = pf_f2bf(e);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+        mrow[i] = mx;
+        lrow[i] = sum;
+      }
+      __syncthreads();
+      pf_f32x4 o[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < ATT_SPLIT / 32; ++st) {
+        const pf_bf16x8 pfr = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&pt[r16][st * 32 + grp * 8]);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              pfr, __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&vt[dt * 16 + r16][st * 32 + grp * 8]), o[dt], 0, 0, 0);
+      }
+      // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int pc = mt * 16 + grp * 4 + i;
+        if (pc >= P) continue;
+        const int row = r0 + prow[pc / G];
+        float *dst = a.part + (((size_t)row * a.n_heads + kvh * G + pc % G) * a.jmax + split) * (HD + 2);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = o[dt][i];
+        if (r16 == 0) { dst[HD] = mrow[i]; dst[HD + 1] = lrow[i]; }
+      }
+      __syncthreads();
+    }
+  };
+
+  if (!any_chain) {
+    // one pass over every row of the group that reaches this split
+    const int mypos = lane < nr ? a.row_pos[r0 + lane] : -1;
+    const unsigned long long b = __ballot(mypos >= s0);
+    if (mypos >= s0) prow[__popcll(b & ((1ull << lane) - 1ull))] = lane;
+    __syncthreads();
+    pass(__popcll(b));
+    return;
+  }
+  for (int rr = 0; rr < nr; ++rr) {
+    const int r = r0 + rr;
+    const int pos = a.row_pos[r], nc = a.row_nc[r], coff = a.row_chain_off[r];
+    if (s0 > pos) continue;
+    __syncthreads();
+    // this row's chain keys and values at positions [max(nc, s0), pos]
+    const int tb = max(nc, s0), te = min(pos, s0 + ATT_SPLIT - 1);
+    if (tb <= te) {
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt) {
+        const int kp = s0 + nt * 16 + r16;
+        if (kp >= tb && kp <= te) {
+          const uint16_t *src = kbase + (size_t)a.chain[coff + (kp - nc)] * HD + grp * 8;
+#pragma unroll
+          for (int st = 0; st < KS; ++st) kf[nt][st] = *(const uint4 *)(src + st * 32);
+        }
+      }
+      for (int e = lane; e < (te - tb + 1) * V4; e += 64) {
+        const int tj = tb + e / V4, c = e % V4;
+        const uint4 w4 = *(const uint4 *)(vbase + (size_t)a.chain[coff + (tj - nc)] * HD + c * 8);
+        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          vt[c * 8 + 2 * q][tj - s0] = (uint16_t)(w[q] & 0xffffu);
+          vt[c * 8 + 2 * q + 1][tj - s0] = (uint16_t)(w[q] >> 16);
+        }
+      }
+    }
+    if (lane == 0) prow[0] = rr;
+    __syncthreads();
+    pass(1);
+  }
+}
+
 hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
   const int G = a.n_heads / a.n_kv_heads;
   if (G < 1 || G > 8 || a.prompt_len < 1) return hipErrorInvalidValue;
@@ -511,6 +720,20 @@ hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
+  if (n_groups <= 0 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
+  dim3 grid(n_groups, a.n_kv_heads, a.jmax);
+  if (dtype == 1 && a.head_dim == 128) {
+    hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+  if (dtype == 1 && a.head_dim == 64) {
+    hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+  return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);
 }
 
 }  // namespace dex
