@@ -507,21 +507,25 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 // ------------------------------------------------------------------------
 // Decode attention on the matrix cores (bf16 caches, head_dim 64 or 128).
 //
-// Same work split and partials as attn_kernel -- one wave per (row group, kv
-// head, split of 64 logical keys), (o, max, sum) per (row, query head,
-// split) -- with the two products on v_mfma_f32_16x16x32_bf16:
-//   S = Q K^T    the (row, query head) pairs of a pass as 16-row tiles, q
-//                rounded to bf16; four 16-key tiles of the split;
+// Same partials as attn_kernel -- (o, max, sum) per (row, query head, split
+// of 64 logical keys) -- with the two products on v_mfma_f32_16x16x32_bf16:
+//   S = Q K^T    the (row, query head) pairs as 16-row tiles, q rounded to
+//                bf16, against the split's four 16-key tiles;
 //   O = P V      P = exp(S - max) rounded to bf16 through an LDS tile, V
-//                transposed into LDS ([dim][key]) once per split.
+//                transposed into LDS ([dim][key]).
 // Each output element of an MFMA depends only on its own pair's row and its
 // key (or dimension) column, and the softmax statistics reduce over the
 // split's keys in a fixed lane order, so a pair gets the same bits whichever
-// pairs share its tile.  Keys whose position lies in a row's lattice chain
-// are patched into the operands for that row alone: a split holding such
-// keys runs one pass per row, any other split one pass over all its rows.
-// Splits are dispatched last-to-first so that the chain splits, which carry
-// the most passes, start first.
+// pairs share its tile.
+//
+// Work items, one wave each, per kv head:
+//   chain items  (row, first or second split holding the row's lattice
+//                chain positions [nc, pos]): the row alone, its keys read
+//                from the committed cache below nc and from its chain
+//                entries from nc on.  A chain spans at most N + 1 <= 33
+//                positions, so two splits.  Dispatched first.
+//   group items  (row group, split without chain keys): every row of the
+//                group that reaches the split, committed keys only.
 template <int HD>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = HD / 32;                 // k-steps of S over head dims
@@ -531,43 +535,87 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   constexpr int VROW = ATT_SPLIT + 8;         // padded V^T / P row (bf16)
   __shared__ __attribute__((aligned(16))) uint16_t vt[HD][VROW];
   __shared__ __attribute__((aligned(16))) uint16_t pt[16][VROW];
-  __shared__ int prow[ATT_MAX_PAIRS];         // group-relative rows of a pass
+  __shared__ int prow[ATT_MAX_PAIRS];         // rows (relative to r0) of the pass
+  __shared__ int ppos[ATT_MAX_PAIRS];         // positions of those rows
 
-  const int gi = blockIdx.x, kvh = blockIdx.y;
-  const int split = a.jmax - 1 - (int)blockIdx.z;
+  const int kvh = blockIdx.y;
   const int lane = threadIdx.x, r16 = lane & 15, grp = lane >> 4;
-  const int r0 = a.grp_row0[gi], nr = a.grp_nrows[gi], seq = a.grp_seq[gi];
   const int G = a.n_heads / a.n_kv_heads;
-  const int s0 = split * ATT_SPLIT;
-  int maxpos = -1, ncmax = 0;
-  bool any_chain = false;
-  for (int r = 0; r < nr; ++r) {
-    const int pos = a.row_pos[r0 + r], nc = a.row_nc[r0 + r];
-    maxpos = max(maxpos, pos);
-    ncmax = max(ncmax, nc);
-    any_chain |= max(nc, s0) <= min(pos, s0 + ATT_SPLIT - 1);
+  const int n_chain_items = 2 * a.n_rows;
+  const int item = blockIdx.x;
+  int r0, seq, split, n_pass;
+  int c_nc = 0, c_pos = -1, c_coff = 0;       // chain item: its row
+  int tn;                                     // group item: committed keys of the split
+  const bool chain_item = item < n_chain_items;
+  if (chain_item) {
+    r0 = item >> 1;
+    c_pos = a.row_pos[r0];
+    c_nc = a.row_nc[r0];
+    c_coff = a.row_chain_off[r0];
+    seq = a.row_seq[r0];
+    if (c_pos < c_nc) return;                 // no chain keys
+    split = c_nc / ATT_SPLIT + (item & 1);
+    if (split * ATT_SPLIT > c_pos) return;
+    n_pass = 1;
+    if (lane == 0) { prow[0] = 0; ppos[0] = c_pos; }
+    tn = 0;
+  } else {
+    const int gi = (item - n_chain_items) / a.jmax;
+    split = a.jmax - 1 - (item - n_chain_items) % a.jmax;
+    r0 = a.grp_row0[gi];
+    seq = a.grp_seq[gi];
+    const int nr = a.grp_nrows[gi];
+    const int s0 = split * ATT_SPLIT, s1 = s0 + ATT_SPLIT - 1;
+    // lane rr holds row rr of the group (at most 64 rows)
+    const bool lr = lane < nr;
+    const int mypos = lr ? a.row_pos[r0 + lane] : -1;
+    const int mync = lr ? a.row_nc[r0 + lane] : 0;
+    int maxpos = mypos, ncmax = mync;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      maxpos = max(maxpos, __shfl_xor(maxpos, o, 64));
+      ncmax = max(ncmax, __shfl_xor(ncmax, o, 64));
+    }
+    if (s0 > maxpos) return;
+    if (__ballot(lr && max(mync, s0) <= min(mypos, s1)) != 0ull) return;   // a chain item's split
+    const unsigned long long reach = __ballot(mypos >= s0);
+    n_pass = __popcll(reach);
+    if (mypos >= s0) {
+      const int k = __popcll(reach & ((1ull << lane) - 1ull));
+      prow[k] = lane;
+      ppos[k] = mypos;
+    }
+    tn = max(0, min(ATT_SPLIT, ncmax - s0));
   }
-  if (s0 > maxpos) return;
+  __syncthreads();
+  const int s0 = split * ATT_SPLIT;
   const uint16_t *kbase = (const uint16_t *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
   const uint16_t *vbase = (const uint16_t *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
-  const int tn = max(0, min(ATT_SPLIT, ncmax - s0));   // committed keys in the split
+  // cache entry of key position s0 + j: committed below nc, then the chain;
+  // -1 past what any row of the item attends to
+  auto entry = [&](int j) -> int {
+    const int kp = s0 + j;
+    if (chain_item) return kp < c_nc ? kp : (kp <= c_pos ? a.chain[c_coff + (kp - c_nc)] : -1);
+    return j < tn ? kp : -1;
+  };
 
   // K as B fragments in registers: kf[nt][st] = key s0 + 16 nt + r16, dims
   // 32 st + 8 grp .. +8
   uint4 kf[NKT][KS];
 #pragma unroll
-  for (int nt = 0; nt < NKT; ++nt)
+  for (int nt = 0; nt < NKT; ++nt) {
+    const int e = entry(nt * 16 + r16);
 #pragma unroll
-    for (int st = 0; st < KS; ++st) {
-      const int j = nt * 16 + r16;
-      kf[nt][st] = j < tn ? *(const uint4 *)(kbase + (size_t)(s0 + j) * HD + st * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
-    }
-  // V: lane j loads key j's row, then writes it as column j of V^T
+    for (int st = 0; st < KS; ++st)
+      kf[nt][st] = e >= 0 ? *(const uint4 *)(kbase + (size_t)e * HD + st * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+  }
+  // V: lane j loads key j's row and writes it as column j of V^T
   {
+    const int e = entry(lane);
     uint4 vv[V4];
 #pragma unroll
     for (int c = 0; c < V4; ++c)
-      vv[c] = lane < tn ? *(const uint4 *)(vbase + (size_t)(s0 + lane) * HD + c * 8) : make_uint4(0, 0, 0, 0);
+      vv[c] = e >= 0 ? *(const uint4 *)(vbase + (size_t)e * HD + c * 8) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int c = 0; c < V4; ++c) {
       const uint32_t w[4] = {vv[c].x, vv[c].y, vv[c].z, vv[c].w};
@@ -578,134 +626,91 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
       }
     }
   }
+  __syncthreads();
 
-  auto pass = [&](int nrp) {
-    const int P = nrp * G;
-    for (int mt = 0; mt * 16 < P; ++mt) {
-      // A fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
-      const int pa = mt * 16 + r16;
-      const bool pok = pa < P;
-      const int prr = pok ? prow[pa / G] : 0;
-      const float *qsrc = a.q + (size_t)(r0 + prr) * a.ldq + (kvh * G + (pok ? pa % G : 0)) * HD + grp * 8;
-      pf_bf16x8 qf[KS];
+  const int P = n_pass * G;
+  for (int mt = 0; mt * 16 < P; ++mt) {
+    // A fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
+    const int pa = mt * 16 + r16;
+    const bool pok = pa < P;
+    const int row = r0 + (pok ? prow[pa / G] : 0);
+    const float *qsrc = a.q + (size_t)row * a.ldq + (kvh * G + (pok ? pa % G : 0)) * HD + grp * 8;
+    pf_bf16x8 qf[KS];
 #pragma unroll
-      for (int st = 0; st < KS; ++st) {
-        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-        if (pok) {
-          x0 = *(const float4 *)(qsrc + st * 32);
-          x1 = *(const float4 *)(qsrc + st * 32 + 4);
-        }
-        uint4 u;
-        u.x = pf_f2bf(x0.x) | ((uint32_t)pf_f2bf(x0.y) << 16);
-        u.y = pf_f2bf(x0.z) | ((uint32_t)pf_f2bf(x0.w) << 16);
-        u.z = pf_f2bf(x1.x) | ((uint32_t)pf_f2bf(x1.y) << 16);
-        u.w = pf_f2bf(x1.z) | ((uint32_t)pf_f2bf(x1.w) << 16);
-        qf[st] = __builtin_bit_cast(pf_bf16x8, u);
+    for (int st = 0; st < KS; ++st) {
+      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+      if (pok) {
+        x0 = *(const float4 *)(qsrc + st * 32);
+        x1 = *(const float4 *)(qsrc + st * 32 + 4);
       }
-      pf_f32x4 sc[NKT];
-#pragma unroll
-      for (int nt = 0; nt < NKT; ++nt) sc[nt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < KS; ++st)
-#pragma unroll
-        for (int nt = 0; nt < NKT; ++nt)
-          sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st], __builtin_bit_cast(pf_bf16x8, kf[nt][st]), sc[nt], 0, 0, 0);
-      // softmax over the split per pair: lane holds pairs mt*16 + 4 grp + i,
-      // keys 16 nt + r16
-      float mrow[4], lrow[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int pc = mt * 16 + grp * 4 + i;
-        const int pos = pc < P ? a.row_pos[r0 + prow[pc / G]] : -1;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int nt = 0; nt < NKT; ++nt) {
-          float v = sc[nt][i] * a.scale;
-          if (s0 + nt * 16 + r16 > pos) v = -INFINITY;
-          sc[nt][i] = v;
-          mx = fmaxf(mx, v);
-        }
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-        float sum = 0.f;
-#pragma unroll
-        for (int nt = 0; nt < NKT; ++nt) {
-          const float e = (mx == -INFINITY) ? 0.f : expf(sc[nt][i] - mx);
-          sum += e;
-          pt[grp * 4 + i][nt * 16 + r16] = pf_f2bf(e);
-        }
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
-        mrow[i] = mx;
-        lrow[i] = sum;
-      }
-      __syncthreads();
-      pf_f32x4 o[DT];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < ATT_SPLIT / 32; ++st) {
-        const pf_bf16x8 pfr = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&pt[r16][st * 32 + grp * 8]);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              pfr, __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&vt[dt * 16 + r16][st * 32 + grp * 8]), o[dt], 0, 0, 0);
-      }
-      // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int pc = mt * 16 + grp * 4 + i;
-        if (pc >= P) continue;
-        const int row = r0 + prow[pc / G];
-        float *dst = a.part + (((size_t)row * a.n_heads + kvh * G + pc % G) * a.jmax + split) * (HD + 2);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = o[dt][i];
-        if (r16 == 0) { dst[HD] = mrow[i]; dst[HD + 1] = lrow[i]; }
-      }
-      __syncthreads();
+      uint4 u;
+      u.x = pf_f2bf(x0.x) | ((uint32_t)pf_f2bf(x0.y) << 16);
+      u.y = pf_f2bf(x0.z) | ((uint32_t)pf_f2bf(x0.w) << 16);
+      u.z = pf_f2bf(x1.x) | ((uint32_t)pf_f2bf(x1.y) << 16);
+      u.w = pf_f2bf(x1.z) | ((uint32_t)pf_f2bf(x1.w) << 16);
+      qf[st] = __builtin_bit_cast(pf_bf16x8, u);
     }
-  };
-
-  if (!any_chain) {
-    // one pass over every row of the group that reaches this split
-    const int mypos = lane < nr ? a.row_pos[r0 + lane] : -1;
-    const unsigned long long b = __ballot(mypos >= s0);
-    if (mypos >= s0) prow[__popcll(b & ((1ull << lane) - 1ull))] = lane;
-    __syncthreads();
-    pass(__popcll(b));
-    return;
-  }
-  for (int rr = 0; rr < nr; ++rr) {
-    const int r = r0 + rr;
-    const int pos = a.row_pos[r], nc = a.row_nc[r], coff = a.row_chain_off[r];
-    if (s0 > pos) continue;
-    __syncthreads();
-    // this row's chain keys and values at positions [max(nc, s0), pos]
-    const int tb = max(nc, s0), te = min(pos, s0 + ATT_SPLIT - 1);
-    if (tb <= te) {
+    pf_f32x4 sc[NKT];
+#pragma unroll
+    for (int nt = 0; nt < NKT; ++nt) sc[nt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt)
+        sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st], __builtin_bit_cast(pf_bf16x8, kf[nt][st]), sc[nt], 0, 0, 0);
+    // softmax over the split per pair: lane holds pairs mt*16 + 4 grp + i,
+    // keys 16 nt + r16
+    float mrow[4], lrow[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pc = mt * 16 + grp * 4 + i;
+      const int pos = pc < P ? ppos[pc / G] : -1;
+      float mx = -INFINITY;
 #pragma unroll
       for (int nt = 0; nt < NKT; ++nt) {
-        const int kp = s0 + nt * 16 + r16;
-        if (kp >= tb && kp <= te) {
-          const uint16_t *src = kbase + (size_t)a.chain[coff + (kp - nc)] * HD + grp * 8;
-#pragma unroll
-          for (int st = 0; st < KS; ++st) kf[nt][st] = *(const uint4 *)(src + st * 32);
-        }
+        float v = sc[nt][i] * a.scale;
+        if (s0 + nt * 16 + r16 > pos) v = -INFINITY;
+        sc[nt][i] = v;
+        mx = fmaxf(mx, v);
       }
-      for (int e = lane; e < (te - tb + 1) * V4; e += 64) {
-        const int tj = tb + e / V4, c = e % V4;
-        const uint4 w4 = *(const uint4 *)(vbase + (size_t)a.chain[coff + (tj - nc)] * HD + c * 8);
-        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          vt[c * 8 + 2 * q][tj - s0] = (uint16_t)(w[q] & 0xffffu);
-          vt[c * 8 + 2 * q + 1][tj - s0] = (uint16_t)(w[q] >> 16);
-        }
+      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      float sum = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt) {
+        const float e = (mx == -INFINITY) ? 0.f : expf(sc[nt][i] - mx);
+        sum += e;
+        pt[grp * 4 + i][nt * 16 + r16] = pf_f2bf(e);
       }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+      mrow[i] = mx;
+      lrow[i] = sum;
     }
-    if (lane == 0) prow[0] = rr;
     __syncthreads();
-    pass(1);
+    pf_f32x4 o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < ATT_SPLIT / 32; ++st) {
+      const pf_bf16x8 pfr = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&pt[r16][st * 32 + grp * 8]);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            pfr, __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&vt[dt * 16 + r16][st * 32 + grp * 8]), o[dt], 0, 0, 0);
+    }
+    // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pc = mt * 16 + grp * 4 + i;
+      if (pc >= P) continue;
+      const int prw = r0 + prow[pc / G];
+      float *dst = a.part + (((size_t)prw * a.n_heads + kvh * G + pc % G) * a.jmax + split) * (HD + 2);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = o[dt][i];
+      if (r16 == 0) { dst[HD] = mrow[i]; dst[HD + 1] = lrow[i]; }
+    }
+    __syncthreads();
   }
 }
 
@@ -725,12 +730,13 @@ hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
 hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
   if (n_groups <= 0 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
   dim3 grid(n_groups, a.n_kv_heads, a.jmax);
-  if (dtype == 1 && a.head_dim == 128) {
-    hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(64), 0, s, a);
-    return hipGetLastError();
-  }
-  if (dtype == 1 && a.head_dim == 64) {
-    hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(64), 0, s, a);
+  if (dtype == 1 && (a.head_dim == 128 || a.head_dim == 64)) {
+    if (a.n_rows < 1 || a.row_seq == nullptr) return hipErrorInvalidValue;
+    const size_t items = 2 * (size_t)a.n_rows + (size_t)n_groups * a.jmax;
+    if (items > 0x7fffffffull) return hipErrorInvalidValue;
+    dim3 g2((unsigned)items, a.n_kv_heads);
+    if (a.head_dim == 128) hipLaunchKernelGGL(attn_mfma_kernel<128>, g2, dim3(64), 0, s, a);
+    else hipLaunchKernelGGL(attn_mfma_kernel<64>, g2, dim3(64), 0, s, a);
     return hipGetLastError();
   }
   return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);

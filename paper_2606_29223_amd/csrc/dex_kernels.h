@@ -88,6 +88,8 @@ struct AttnArgs {
   // row groups: consecutive rows of one sequence
   const int *grp_row0, *grp_nrows, *grp_seq;
   const int *row_pos, *row_nc, *row_chain_off, *chain;
+  const int *row_seq;         // sequence of each row (matrix-core kernel)
+  int n_rows;                 // rows of the launch (matrix-core kernel)
   float *part;                // [R][H][jmax][hd + 2] split partials (o, max, sum)
   int jmax;
   float scale;

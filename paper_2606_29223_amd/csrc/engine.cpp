@@ -309,6 +309,7 @@ dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, cons
       a.kv_entries = ctx->E; a.n_kv_heads = Hkv; a.n_heads = H; a.head_dim = hd; a.batch = ctx->B;
       a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq;
       a.row_pos = t.pos; a.row_nc = t.nc; a.row_chain_off = t.chain_off; a.chain = t.chain;
+      a.row_seq = t.seq; a.n_rows = M;
       a.part = apart; a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
       TimedLaunch tl(ctx, 1, t.attn_bytes);
       HIPCHK(launch_attention(ctx->dtype, a, t.n_groups, st));
@@ -706,6 +707,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.kv_entries = ctx->E; a.n_kv_heads = ctx->Hkv; a.n_heads = H; a.head_dim = hd; a.batch = B;
       a.grp_row0 = d_grel + g_first; a.grp_nrows = d_gn + g_first; a.grp_seq = d_gs + g_first;
       a.row_pos = d_pos + c0; a.row_nc = d_nc + c0; a.row_chain_off = d_coff + c0; a.chain = d_zero;
+      a.row_seq = d_seq + c0; a.n_rows = cn;
       a.part = apart; a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
       HIPCHK(launch_attention(ctx->dtype, a, g_cnt, ctx->stream));
       CombineArgs cb{};
@@ -851,7 +853,9 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     stage_g0[k] = ngroups;
     for (int r = stage_r0[k]; r < stage_r0[k + 1];) {
       int e = r;
-      while (e < stage_r0[k + 1] && rows[e].seq == rows[r].seq && e - r < grp_rows) ++e;
+      // (the rows of a group share their committed prefix: the attention
+      // kernels rely on it)
+      while (e < stage_r0[k + 1] && rows[e].seq == rows[r].seq && t_nc[e] == t_nc[r] && e - r < grp_rows) ++e;
       t_g0[ngroups] = r - stage_r0[k];
       t_gn[ngroups] = e - r;
       t_gs[ngroups] = rows[r].seq;
