@@ -108,6 +108,10 @@ typedef struct {
   int32_t batch;                        /* independent sequences, 1 .. DEX_MAX_BATCH */
   int32_t max_context;                  /* prompt length + generated tokens, per sequence */
   void *hip_stream;                     /* hipStream_t or NULL */
+  int32_t stage_streams;                /* streams a round's stages are spread over: the
+                                           stages of one round read and write disjoint
+                                           state, so they may run concurrently.  0: the
+                                           library default; 1: everything on hip_stream */
 } dex_config;
 
 /* What one dex_step did (all host memory).  Rows are listed stage-major,

@@ -11,7 +11,8 @@
 //                 [B][2S][d/16] of each slot's last completed stage, and its
 //                 candidate tokens int [B][2S][N].
 //   round scratch rows x {h, partials, norm input, q, attention out, SwiGLU
-//                 out}, attention split partials, LM-head tile winners.
+//                 out}, attention split partials, LM-head tile winners; a
+//                 stage works in its own row range, so stages may overlap.
 // One host->device copy of the round's row tables, one device->host copy of
 // the decoded candidates and commits per round.
 #include <algorithm>
@@ -28,6 +29,9 @@
 using namespace dex;
 
 namespace {
+
+// streams a round's stages are spread over unless the caller says otherwise
+constexpr int kDefaultStageStreams = 4;
 
 thread_local std::string g_create_error;
 
@@ -78,6 +82,11 @@ struct dex_ctx {
   std::vector<int> X;
   int N, W, decs, B, max_ctx;
   hipStream_t stream;
+  // stage lanes: lane 0 is `stream`, the others library-owned streams
+  int n_lanes = 1;
+  std::vector<hipStream_t> lane_st;
+  std::vector<hipEvent_t> lane_ev;
+  hipEvent_t fork_ev = nullptr;
   std::vector<std::vector<int>> stage_layers;
   // capacities
   int S, R_max, CH_MAX, E, n_part, jmax;
@@ -279,10 +288,9 @@ struct StageTables {
 
 double wbytes(const dex_ctx *ctx, double elems) { return elems * ctx->es; }
 
-dex_status run_layers(dex_ctx *ctx, int first_layer, int last_layer, int M, const StageTables &t,
+dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_layer, int M, const StageTables &t,
                       float *h, float *part, void *xb, float *q, void *att, void *act, float *apart,
                       int jmax, bool to_boundary, const int *bnd_rows) {
-  const hipStream_t st = ctx->stream;
   const int d = ctx->d, H = ctx->H, Hkv = ctx->Hkv, hd = ctx->hd, F = ctx->F;
   const size_t layer_kv = (size_t)ctx->B * Hkv * ctx->E * hd * ctx->es;
   for (int l = first_layer; l <= last_layer; ++l) {
@@ -420,6 +428,12 @@ void dex_destroy(dex_ctx *ctx) {
   if (ctx->res_host) (void)hipHostFree(ctx->res_host);
   if (ctx->job_host) (void)hipHostFree(ctx->job_host);
   for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
+  for (size_t i = 1; i < ctx->lane_st.size(); ++i) {
+    (void)hipStreamSynchronize(ctx->lane_st[i]);
+    (void)hipStreamDestroy(ctx->lane_st[i]);
+  }
+  for (auto e : ctx->lane_ev) if (e) (void)hipEventDestroy(e);
+  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
   delete ctx;
 }
 
@@ -574,6 +588,24 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       g_create_error = ctx->err;
       dex_destroy(ctx);
       return ps;
+    }
+  }
+  // stage lanes (default priority, non-blocking streams)
+  {
+    ctx->n_lanes = c->stage_streams > 0 ? std::min<int>(c->stage_streams, 8) : kDefaultStageStreams;
+    ctx->lane_st.assign(ctx->n_lanes, ctx->stream);
+    ctx->lane_ev.assign(ctx->n_lanes, nullptr);
+    hipError_t e = hipSuccess;
+    if (ctx->n_lanes > 1) e = hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming);
+    for (int i = 1; i < ctx->n_lanes && e == hipSuccess; ++i) {
+      e = hipStreamCreateWithFlags(&ctx->lane_st[i], hipStreamNonBlocking);
+      if (e != hipSuccess) { ctx->lane_st[i] = nullptr; ctx->lane_st.resize(i); break; }
+      e = hipEventCreateWithFlags(&ctx->lane_ev[i], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      g_create_error = std::string("stream creation failed: ") + hipGetErrorString(e);
+      dex_destroy(ctx);
+      return DEX_E_HIP;
     }
   }
   ctx->seqs.resize(ctx->B);
@@ -879,10 +911,22 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   auto dptr = [&](const int *hp) { return D + (hp - T); };
 
   // ------------------------------------------------------------ sweep
-  int layers_streamed = 0, row_layers = 0;
+  // The stages of a round are independent: each row reads the boundary
+  // state its slot reached in an earlier round, writes its own slot's, and
+  // touches the key/value cache only in its own stage's layers.  Each stage
+  // works in its own row range of the scratch buffers, so the stages can be
+  // spread over the lanes; the exit heads wait for all of them.  (Per-kernel
+  // timing keeps everything on one stream.)
+  const bool multi = ctx->n_lanes > 1 && !ctx->timing;
+  if (multi) {
+    HIPCHK(hipEventRecord(ctx->fork_ev, ctx->stream));
+    for (int i = 1; i < ctx->n_lanes; ++i) HIPCHK(hipStreamWaitEvent(ctx->lane_st[i], ctx->fork_ev, 0));
+  }
+  int layers_streamed = 0, row_layers = 0, lane_next = 0;
   for (int k = 0; k < N; ++k) {
     const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
     if (M == 0) continue;
+    const hipStream_t lst = multi ? ctx->lane_st[lane_next++ % ctx->n_lanes] : ctx->stream;
     const std::vector<int> &ls = ctx->stage_layers[k];
     layers_streamed += (int)ls.size();
     row_layers += M * (int)ls.size();
@@ -903,13 +947,26 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
       p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
       p.row_tok = t.tok; p.row_src = t.bnd; p.embed = ctx->embed; p.bnd_h = ctx->bnd_h; p.bnd_part = ctx->bnd_part;
       p.g = (const float *)LW(ctx, ls.front(), DEX_P_ATTN_NORM);
-      p.h = ctx->h_w; p.part = ctx->part_w; p.xb = ctx->xb_w;
+      p.h = ctx->h_w + (size_t)r0 * ctx->d; p.part = ctx->part_w + (size_t)r0 * ctx->n_part;
+      p.xb = (char *)ctx->xb_w + (size_t)r0 * ctx->d * ctx->es;
       TimedLaunch tl(ctx, 7, 0.0);
-      HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
+      HIPCHK(launch_prep(ctx->dtype, p, lst));
     }
-    dex_status rs = run_layers(ctx, ls.front(), ls.back(), M, t, ctx->h_w, ctx->part_w, ctx->xb_w, ctx->q_w,
-                               ctx->att_w, ctx->act_w, ctx->attn_part, ctx->jmax, true, t.bnd);
+    dex_status rs = run_layers(ctx, lst, ls.front(), ls.back(), M, t, ctx->h_w + (size_t)r0 * ctx->d,
+                               ctx->part_w + (size_t)r0 * ctx->n_part,
+                               (char *)ctx->xb_w + (size_t)r0 * ctx->d * ctx->es,
+                               ctx->q_w + (size_t)r0 * ctx->H * ctx->hd,
+                               (char *)ctx->att_w + (size_t)r0 * ctx->H * ctx->hd * ctx->es,
+                               (char *)ctx->act_w + (size_t)r0 * ctx->F * ctx->es,
+                               ctx->attn_part + (size_t)r0 * ctx->H * ctx->jmax * (ctx->hd + 2), ctx->jmax,
+                               true, t.bnd);
     if (rs != DEX_OK) return fail(ctx, rs);
+  }
+  if (multi) {
+    for (int i = 1; i < ctx->n_lanes; ++i) {
+      HIPCHK(hipEventRecord(ctx->lane_ev[i], ctx->lane_st[i]));
+      HIPCHK(hipStreamWaitEvent(ctx->stream, ctx->lane_ev[i], 0));
+    }
   }
   // ---------------------------------------------------- exit + commit
   dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),

@@ -45,6 +45,7 @@ class DexConfig(ctypes.Structure):
         ("explored", ctypes.POINTER(ctypes.c_int32)), ("n_explored", ctypes.c_int32),
         ("width_cap", ctypes.c_int32), ("decs", ctypes.c_int32), ("batch", ctypes.c_int32),
         ("max_context", ctypes.c_int32), ("hip_stream", ctypes.c_void_p),
+        ("stage_streams", ctypes.c_int32),
     ]
 
 
@@ -168,7 +169,7 @@ class Decoder:
     """One library context over device-resident weights."""
 
     def __init__(self, cfg: dict, dev_weights: dict, explored=None, width_cap=None, decs=None,
-                 batch=None, max_context=None, stream=None):
+                 batch=None, max_context=None, stream=None, stage_streams=0):
         import torch
         self.lib = load()
         self.cfg = cfg
@@ -201,6 +202,7 @@ class Decoder:
         # legacy null stream would also order against every other stream
         self.stream = stream if stream is not None else torch.cuda.Stream()
         c.hip_stream = self.stream.cuda_stream
+        c.stage_streams = int(stage_streams)
         torch.cuda.synchronize()                # weights uploaded on other streams are complete
         self.model_struct, self.config_struct = m, c
         self.max_context = c.max_context
