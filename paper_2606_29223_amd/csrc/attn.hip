@@ -232,10 +232,24 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 template <typename T, int HD>
 __global__ __launch_bounds__(64) void combine_kernel(CombineArgs a) {
   constexpr int DPL = HD >= 64 ? HD / 64 : 1;
-  __shared__ float ws[ATT_MAX_SPLITS];
+  constexpr int CH = 16;                       // splits per value chunk
+  extern __shared__ float ws[];                // [jmax] split weights
   const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
   const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (HD + 2);
+  const int d0 = lane * DPL;
+  const bool dok = d0 < HD;
+  // the split values do not depend on the statistics: the first chunk is
+  // requested before them, each next chunk before the current one is summed
+  float va[CH][DPL], vb[CH][DPL];
+  auto load_chunk = [&](int j0, float (&v)[CH][DPL]) {
+#pragma unroll
+    for (int jj = 0; jj < CH; ++jj)
+#pragma unroll
+      for (int q = 0; q < DPL; ++q)
+        v[jj][q] = (dok && j0 + jj < nsplit) ? src[(size_t)(j0 + jj) * (HD + 2) + d0 + q] : 0.f;
+  };
+  load_chunk(0, va);
   float M = -INFINITY;
   for (int j0 = 0; j0 < nsplit; j0 += 64) {
     const int j = j0 + lane;
@@ -254,26 +268,26 @@ __global__ __launch_bounds__(64) void combine_kernel(CombineArgs a) {
     lsum += wave_sum(w * lj);
   }
   __syncthreads();
-  const int d0 = lane * DPL;
-  if (d0 >= HD) return;
   float o[DPL];
 #pragma unroll
   for (int q = 0; q < DPL; ++q) o[q] = 0.f;
-  for (int j0 = 0; j0 < nsplit; j0 += 8) {
-    float v[8][DPL];
+  auto sum_chunk = [&](int j0, const float (&v)[CH][DPL]) {
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
-#pragma unroll
-      for (int q = 0; q < DPL; ++q)
-        v[jj][q] = (j0 + jj < nsplit) ? src[(size_t)(j0 + jj) * (HD + 2) + d0 + q] : 0.f;
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
+    for (int jj = 0; jj < CH; ++jj) {
       if (j0 + jj >= nsplit) break;
       const float w = ws[j0 + jj];
 #pragma unroll
       for (int q = 0; q < DPL; ++q) o[q] = fmaf(w, v[jj][q], o[q]);
     }
+  };
+  for (int j0 = 0; j0 < nsplit; j0 += 2 * CH) {
+    if (j0 + CH < nsplit) load_chunk(j0 + CH, vb);
+    sum_chunk(j0, va);
+    if (j0 + CH >= nsplit) break;
+    if (j0 + 2 * CH < nsplit) load_chunk(j0 + 2 * CH, va);
+    sum_chunk(j0 + CH, vb);
   }
+  if (!dok) return;
   T *out = (T *)a.out + (size_t)r * a.ld_out + h * HD + d0;
 #pragma unroll
   for (int q = 0; q < DPL; ++q) {
@@ -302,9 +316,9 @@ static hipError_t launch_attn_t(const AttnArgs &a, dim3 grid, hipStream_t s) {
 template <typename T>
 static hipError_t launch_comb_t(const CombineArgs &a, dim3 grid, hipStream_t s) {
   switch (a.head_dim) {
-    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64), a.jmax * 4, s, a); break;
+    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64), a.jmax * 4, s, a); break;
+    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64), a.jmax * 4, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

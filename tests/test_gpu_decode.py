@@ -283,3 +283,28 @@ def test_small_bf16_prefill_ragged_prompts(P):
                     assert max_rel_err(rd["logits"][r], z[pos - P, 0]) <= LOGIT_RTOL
                     seen += 1
         assert seen == T - 1
+
+
+def test_stage_streams_do_not_change_results():
+    """Spreading a round's stages over several streams changes only the
+    schedule: tokens, lattice traces and every row's exit logits are the same
+    bits as with all stages on one stream (batch 3, width 4, 12 layers)."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = configs.get(SMALL, batch=3, prompt_seeds=[8101, 8102, 8103])
+    prompt = gen.prompts(cfg)
+    T = 24
+    out = []
+    for lanes in (1, 4):
+        dec = dexlib.Decoder(cfg, device_weights(SMALL), max_context=cfg["prompt_len"] + T, stage_streams=lanes)
+        tap = torch.empty((dec.batch * cfg["width_cap"], cfg["vocab"]), dtype=torch.float32, device="cuda")
+        dec.set_logits_tap(tap)
+        out.append(_run(dec, prompt, T, tap=tap))
+        dec.close()
+    (t1, r1), (t4, r4) = out
+    assert np.array_equal(t1, t4)
+    assert len(r1) == len(r4)
+    for a, b in zip(r1, r4):
+        assert a["rows"] == b["rows"] and a["kstar"] == b["kstar"] and a["collapse"] == b["collapse"]
+        assert all(np.array_equal(x, y) for x, y in zip(a["lattice"], b["lattice"]))
+        assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
