@@ -34,13 +34,17 @@ SHORT = {
 
 
 def gemm_source_hash() -> str:
+    """Hash of the decode GEMM kernel source and of its argument struct."""
     h = hashlib.sha1()
-    for f in ("gemm.hip", "dex_kernels.h"):
-        h.update(open(os.path.join(PKG, "csrc", f), "rb").read())
+    h.update(open(os.path.join(PKG, "csrc", "gemm.hip"), "rb").read())
+    hdr = open(os.path.join(PKG, "csrc", "dex_kernels.h")).read()
+    start = hdr.index("struct GemmArgs {")
+    h.update(hdr[start:hdr.index("};", start)].encode())
     return h.hexdigest()[:16]
 
 
 def _short(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "")
     base = name.split("(")[0].replace("void ", "").replace("dex::", "")
     return base
 
@@ -54,7 +58,7 @@ def stats(args):
         lines.append(f"{_short(r['Name'])[:58]:58s} {r['Calls']:>7s} {float(r['AverageNs']) / 1e3:9.2f} "
                      f"{float(r['TotalDurationNs']) / 1e6:9.2f} {float(r['Percentage']):6.1f}")
     if trace:
-        lines += ["", "decode launches (median duration; decode = M <= 16 GEMMs, attention grid x <= 256)"]
+        lines += ["", "decode launches (median duration; decode = M <= 16 GEMMs and the decode attention kernels)"]
         groups = {}
         for t in trace:
             n = _short(t["Kernel_Name"])
@@ -63,7 +67,7 @@ def stats(args):
             for k, v in SHORT.items():
                 if n.startswith(k):
                     key = v
-            if n.startswith("attn_kernel") and int(t["Grid_Size_X"]) <= 256 * 64:
+            if n.startswith("attn_mfma_kernel") or (n.startswith("attn_kernel") and int(t["Grid_Size_X"]) <= 256 * 64):
                 key = "attention (decode)"
             if n.startswith("combine_kernel") and int(t["Grid_Size_X"]) <= 256 * 64:
                 key = "attention combine (decode)"
