@@ -12,8 +12,11 @@ Prints one JSON line.  Besides the contract fields it carries
                around back-to-back launches at the most common rows-per-stage,
                against the 8 TB/s HBM peak;
   dex          lattice statistics: rounds and layers per committed token,
-               algorithmic bytes per commit and the resulting HBM-roofline
+               matched-depth histogram, algorithmic bytes per commit (weights
+               of the stages each round ran, the exit head, and the
+               attention's key/value reads) and the resulting HBM-roofline
                tokens/s of this schedule;
+  e2e          committed tokens/s including the prefill (y_0 counts);
   cpu_baseline the oracle (float64 numpy) running the same decode on the host
                cores for a bounded sample.
 """
@@ -107,10 +110,15 @@ def main():
         max_ctx = P + need
 
     dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx)
+    torch.cuda.synchronize()
+    tp = time.perf_counter()
     dec.prefill(prompts)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - tp
     B = dec.batch
 
     m_hist = {}
+    kstar_hist = {}
 
     def steps(n):
         commits = rounds = layers = row_layers = 0
@@ -124,15 +132,27 @@ def main():
                 mk = dec.info.rows_per_stage[k]
                 if mk:
                     m_hist[mk] = m_hist.get(mk, 0) + 1
+            for b in range(B):
+                ks = dec.info.kstar[b]
+                if ks >= 0:
+                    kstar_hist[ks] = kstar_hist.get(ks, 0) + 1
         return commits, rounds, layers, row_layers
 
-    steps(args.warmup)
+    tw = time.perf_counter()
+    warm_commits = steps(args.warmup)[0]
     torch.cuda.synchronize()
+    warm_s = time.perf_counter() - tw
+    m_hist.clear()
+    kstar_hist.clear()
     t0 = time.perf_counter()
     commits, rounds, layers, row_layers = steps(args.steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     value = commits / elapsed
+    # end to end as the paper counts it: y_0 of every sequence from the
+    # prefill plus every commit, over prefill and all decode rounds so far
+    e2e = (B + warm_commits + commits) / (prefill_s + warm_s + elapsed)
+    kstar_timed = dict(kstar_hist)
 
     # instrumented run of the same length: per-kernel HIP event durations
     # (each launch bracketed by events; includes the event overhead)
@@ -141,6 +161,7 @@ def main():
     torch.cuda.synchronize()
     ms, n, nbytes = dec.kernel_times()
     dec.set_timing(False)
+    attn_bytes_per_round = nbytes[1] / max(args.steps, 1)   # K/V, q and outputs of the attention
     names = dexlib.KERNEL_CLASSES
     per_kernel = {names[i]: {"ms": round(ms[i], 3), "launches": int(n[i]),
                              "avg_us_event": round(ms[i] / max(n[i], 1) * 1e3, 2),
@@ -191,6 +212,7 @@ def main():
     layer_bytes = es * (d * (cfg["n_heads"] + 2 * cfg["n_kv_heads"]) * cfg["head_dim"]
                         + cfg["n_heads"] * cfg["head_dim"] * d + 3 * d * F)
     bytes_per_commit = (layers * layer_bytes + rounds * es * V * d) / max(commits, 1)
+    hbm_bytes_per_commit = bytes_per_commit + attn_bytes_per_round * rounds / max(commits, 1)
     cpu = None
     if not args.no_cpu_baseline:
         del dev_w
@@ -220,10 +242,14 @@ def main():
                 "critical_path_layers_per_commit": round(L / N * rounds / max(commits, 1), 3),
                 "ar_layers_per_commit": L,
                 "rows_per_stage_hist": {str(k): v for k, v in sorted(m_hist.items())},
+                "matched_depth_hist": {str(k): v for k, v in sorted(kstar_timed.items())},
                 "weight_bytes_per_commit": bytes_per_commit,
-                "roofline_tokens_per_s": round(PEAK_HBM_GBS * 1e9 / bytes_per_commit, 2),
-                "frac_of_schedule_roofline": round(value * bytes_per_commit / (PEAK_HBM_GBS * 1e9), 4),
-                "achieved_weight_GBps": round(value * bytes_per_commit / 1e9, 1)},
+                "hbm_bytes_per_commit": hbm_bytes_per_commit,
+                "roofline_tokens_per_s": round(PEAK_HBM_GBS * 1e9 / hbm_bytes_per_commit, 2),
+                "frac_of_schedule_roofline": round(value * hbm_bytes_per_commit / (PEAK_HBM_GBS * 1e9), 4),
+                "achieved_GBps": round(value * hbm_bytes_per_commit / 1e9, 1)},
+        "prefill_s": round(prefill_s, 3),
+        "e2e_tokens_per_s": round(e2e, 3),
         "ar_tokens_per_s": round(ar_value, 3) if ar_value else None,
         "kernels": per_kernel,
         "setup_s": round(setup_s, 1),

@@ -4,6 +4,8 @@
       --command "..." --out profiles/NAME.txt
   python3 -m paper_2606_29223_amd.profile_summary traffic FETCH_DIR WRITE_DIR \
       --command "..." --out-json profiles/traffic.json --out profiles/NAME.txt
+  python3 -m paper_2606_29223_amd.profile_summary mfma PMC_DIR --command "..." \
+      --out profiles/NAME.txt
 
 `stats` lists the kernels by total time and, for the decode GEMMs and the
 attention kernels, the median duration of their decode launches.  `traffic`
@@ -142,6 +144,41 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def mfma(args):
+    """Matrix-core utilisation per kernel from one --pmc pass with
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 and
+    GRBM_GUI_ACTIVE: busy cycles summed over the SIMDs over active cycles x
+    SIMDs (GRBM_GUI_ACTIVE reads as the sum of the per-XCD instances, hence
+    the division by --xcds), and achieved bf16 matrix flops (MOPS x 512) over
+    the kernels' duration."""
+    rows = _counter_rows(args.pmc_dir)
+    per = {}
+    for r in rows:
+        key = (r["Dispatch_Id"], _short(r["Kernel_Name"]))
+        d = per.setdefault(key, {"dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    agg = {}
+    for (_, name), d in per.items():
+        a = agg.setdefault(name, {"n": 0, "busy": 0.0, "gui": 0.0, "mops": 0.0, "dur": 0.0})
+        a["n"] += 1
+        a["busy"] += d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        a["gui"] += d.get("GRBM_GUI_ACTIVE", 0.0)
+        a["mops"] += d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        a["dur"] += d["dur"]
+    simds = args.simds
+    lines = [f"command: {args.command}", "",
+             f"matrix-core utilisation per kernel ({simds} SIMDs; util = MFMA busy cycles / (active cycles x SIMDs),",
+             f"active cycles = GRBM_GUI_ACTIVE / {args.xcds} XCD instances;",
+             "bf16 TFLOP/s = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 / kernel time; dense bf16 peak 2500 TFLOP/s)", "",
+             f"{'kernel':44s} {'launches':>8s} {'time_ms':>9s} {'mfma_util_%':>11s} {'bf16_TFLOP/s':>12s}"]
+    for name, a in sorted(agg.items(), key=lambda kv: -kv[1]["dur"])[: args.top]:
+        util = 100.0 * a["busy"] / (a["gui"] / args.xcds * simds) if a["gui"] else 0.0
+        tf = a["mops"] * 512 / a["dur"] / 1e12 if a["dur"] else 0.0
+        lines.append(f"{name[:44]:44s} {a['n']:8d} {a['dur'] * 1e3:9.2f} {util:11.2f} {tf:12.2f}")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -160,8 +197,15 @@ def main():
     t.add_argument("--command", required=True)
     t.add_argument("--out-json", required=True)
     t.add_argument("--out", required=True)
+    m = sub.add_parser("mfma")
+    m.add_argument("pmc_dir")
+    m.add_argument("--command", required=True)
+    m.add_argument("--out", required=True)
+    m.add_argument("--simds", type=int, default=1024)
+    m.add_argument("--xcds", type=int, default=8)
+    m.add_argument("--top", type=int, default=12)
     a = ap.parse_args()
-    stats(a) if a.cmd == "stats" else traffic(a)
+    {"stats": stats, "traffic": traffic, "mfma": mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
