@@ -4,12 +4,13 @@ TEST INFRASTRUCTURE ONLY: imported by tests/, the smoke check and the
 benchmark's CPU-baseline leg, never by the product path.  It shares no code
 with the GPU library; both read the same seeded inputs from synth/.
 
-Modules: model (the synthetic decoder and exit heads), ar (greedy AR and
+Modules: model (the synthetic decoder and exit heads), ar (AR decoding and
 teacher-forced exit logits), lattice (Algorithm 1 / Section 3.2 bookkeeping
-with Algorithm 2's masks), dex (the full procedure on the model), ead
-(Section 2's accounting, used as test pins).
+with Algorithm 2's masks), dex (the full procedure on the model), gumbel
+(Algorithm 2's sampling-mode noise and decode rule), ead (Section 2's
+accounting, used as test pins).
 """
-from . import ar, dex, ead, lattice, model  # noqa: F401
+from . import ar, dex, ead, gumbel, lattice, model  # noqa: F401
 from .model import Model  # noqa: F401
 
 

@@ -45,16 +45,20 @@ def decode_row(model: Model, cache: Cache, token: int, pos: int, layers=None, h=
     return hs
 
 
-def ar_generate(model: Model, prompt, T: int, prefill=None):
-    """Greedy AR.  Returns the T generated tokens y_0..y_{T-1}."""
+def ar_generate(model: Model, prompt, T: int, prefill=None, temperature: float = 0.0, seed: int = 0,
+                seq: int = 0):
+    """Plain AR: greedy, or (temperature > 0) Gumbel-max sampling with the row
+    of (seed, seq, position) at every position (oracle/gumbel.py).  Returns
+    the T generated tokens y_0..y_{T-1}."""
+    from .gumbel import decode
     P = len(prompt)
     Ks, Vs, h_last = prefill if prefill is not None else model.prefill(prompt)
     cache = Cache(model, Ks, Vs, P + T)
-    toks = [argmax_lowest(model.exit_logits(h_last))]
+    toks = [decode(model.exit_logits(h_last), (), temperature, seed, seq, P - 1)]
     for t in range(1, T):
         pos = P + t - 1
         hs = decode_row(model, cache, toks[-1], pos)
-        toks.append(argmax_lowest(model.exit_logits(hs[-1])))
+        toks.append(decode(model.exit_logits(hs[-1]), (), temperature, seed, seq, pos))
     return toks
 
 

@@ -22,8 +22,9 @@ from dataclasses import dataclass, field
 import numpy as np
 
 from .ar import Cache
+from .gumbel import decode
 from .lattice import Lattice
-from .model import Model, argmax_lowest
+from .model import Model
 
 
 @dataclass
@@ -66,8 +67,12 @@ def validate_explored(explored, L):
 
 def dex_generate(model: Model, prompt, explored, width_cap: int, decs: bool, T: int,
                  max_context: int | None = None, force=None, prefill=None, keep_trace=True,
-                 check=None):
+                 check=None, temperature: float = 0.0, seed: int = 0, seq: int = 0):
     """Run DEX until T tokens are generated (y_0 from the prefill included).
+
+    temperature > 0 selects Algorithm 2's sampling mode: every node decodes
+    argmax(l / temperature + G) with the Gumbel row of (seed, seq, its
+    position) (oracle/gumbel.py); 0 is greedy.
 
     force(prefix_tokens, stage, natural_token, mask) may return a token that
     replaces a node's candidate (used by the brute-force test to steer the
@@ -82,7 +87,7 @@ def dex_generate(model: Model, prompt, explored, width_cap: int, decs: bool, T: 
     Ks, Vs, h_last = prefill if prefill is not None else model.prefill(prompt)
     cache = Cache(model, Ks, Vs, max_context)
     committed = list(int(t) for t in prompt)
-    y0 = argmax_lowest(model.exit_logits(h_last))
+    y0 = decode(model.exit_logits(h_last), (), temperature, seed, seq, P - 1)
     committed.append(y0)
     out = [y0]
     lat = Lattice(N, width_cap, bool(decs), max_context, y0, P)
@@ -105,7 +110,7 @@ def dex_generate(model: Model, prompt, explored, width_cap: int, decs: bool, T: 
             s.state["h"] = h
             z = model.exit_logits(h)
             m = lat.mask(s, k)
-            tok = argmax_lowest(z, m)
+            tok = decode(z, m, temperature, seed, seq, s.pos)
             if force is not None:
                 prefix = committed + [a.x for a in chain[1:]] + ([s.x] if s is not lat.anchor else [])
                 # prefix ends with the slot's own input (the anchor's input is committed[-1])
