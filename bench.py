@@ -48,11 +48,14 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=20.0)
     p.add_argument("--no-ar", action="store_true", help="skip the plain AR reference rate")
+    p.add_argument("--temperature", type=float, default=0.0,
+                   help="> 0: Algorithm 2's sampling mode (Gumbel-max, seed --seed); 0: greedy")
+    p.add_argument("--seed", type=int, default=0)
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     return p.parse_args()
 
 
-def cpu_baseline(cfg, weights, prompts, budget_s):
+def cpu_baseline(cfg, weights, prompts, budget_s, temperature=0.0, seed=0):
     """The oracle as it stands, timed on this host: DEX rounds on the first
     sequence after its prefill (prefill untimed)."""
     import oracle
@@ -70,7 +73,7 @@ def cpu_baseline(cfg, weights, prompts, budget_s):
     while True:
         t0 = time.perf_counter()
         r = dex.dex_generate(m, prompt, cfg["explored"], cfg["width_cap"], bool(cfg["decs"]), T,
-                             prefill=pf, keep_trace=False)
+                             prefill=pf, keep_trace=False, temperature=temperature, seed=seed)
         dt = time.perf_counter() - t0
         t_used, commits, rounds = dt, T - 1, r.rounds
         if dt * 2.5 > budget_s or T >= cfg["gen_len"]:
@@ -109,7 +112,8 @@ def main():
     if need > cfg["gen_len"]:
         max_ctx = P + need
 
-    dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx)
+    samp = dict(temperature=args.temperature, seed=args.seed)
+    dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx, **samp)
     torch.cuda.synchronize()
     tp = time.perf_counter()
     dec.prefill(prompts)
@@ -193,7 +197,7 @@ def main():
 
     ar_value = None
     if not args.no_ar:
-        ar = dexlib.Decoder(cfg, dev_w, explored=[cfg["n_layers"]], width_cap=1, max_context=max_ctx)
+        ar = dexlib.Decoder(cfg, dev_w, explored=[cfg["n_layers"]], width_cap=1, max_context=max_ctx, **samp)
         ar.prefill(prompts)
         for _ in range(args.warmup):
             ar.step()
@@ -217,7 +221,7 @@ def main():
     if not args.no_cpu_baseline:
         del dev_w
         torch.cuda.empty_cache()
-        cpu = cpu_baseline(cfg, weights, prompts, args.cpu_seconds)
+        cpu = cpu_baseline(cfg, weights, prompts, args.cpu_seconds, args.temperature, args.seed)
 
     out = {
         "metric": "committed tokens/s at batch 1 (32L d4096 bf16) + achieved HBM GB/s vs peak",
@@ -233,7 +237,9 @@ def main():
         "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
         "data": "synthetic (seeded random weights and uniform prompts)",
         "config": {"workload": cfg["name"], "explored": cfg["explored"], "width_cap": cfg["width_cap"],
-                   "batch": B, "prompt_len": P, "parallelism": "single GPU"},
+                   "batch": B, "prompt_len": P, "parallelism": "single GPU",
+                   "decoding": (f"sampling, temperature {args.temperature}, seed {args.seed}"
+                                if args.temperature > 0 else "greedy")},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "dex": {"commits": commits, "rounds": rounds, "rounds_per_commit": round(rounds / max(commits, 1), 4),

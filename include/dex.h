@@ -112,6 +112,12 @@ typedef struct {
                                            stages of one round read and write disjoint
                                            state, so they may run concurrently.  0: the
                                            library default; 1: everything on hip_stream */
+  float temperature;                    /* 0: greedy decoding.  > 0: Algorithm 2's sampling
+                                           mode, every node decodes argmax(l / temperature
+                                           + G) with G the Gumbel row of (sample_seed,
+                                           sequence, position of the node's input token)
+                                           (see dex_debug_gumbel below) */
+  uint64_t sample_seed;
 } dex_config;
 
 /* What one dex_step did (all host memory).  Rows are listed stage-major,
@@ -207,6 +213,20 @@ dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t r
  * 8 (bf16) or 4 (fp32).  Device pointers.                                   */
 dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M,
                           float *y, void *hip_stream);
+
+/* The Gumbel source of sampling mode (Algorithm 2 draws one Gumbel row per
+ * sampling slot; here the row of a slot is a function of (seed, sequence,
+ * position of the slot's input token), so plain autoregressive sampling at
+ * the same position draws the same row and the committed tokens equal AR
+ * sampling's).  With the SplitMix64 finaliser mix64 and gamma =
+ * 0x9E3779B97F4A7C15 (Steele, Lea and Flood, OOPSLA 2014), all mod 2^64:
+ *   key = mix64(seed ^ mix64(seq * 2^32 + pos)),
+ *   z_v = mix64(key + (v + 1) * gamma),
+ *   u_v = ((z_v >> 41) + 1/2) / 2^23      (exact in binary32),
+ *   G_v = -ln(-ln u_v)                    (binary32 here).
+ * dex_debug_gumbel writes G_0..G_{V-1} of one row to device memory `out`
+ * (float32) on `hip_stream`, for tests of the generator.                    */
+dex_status dex_debug_gumbel(uint64_t seed, int32_t seq, int32_t pos, int32_t V, float *out, void *hip_stream);
 
 /* Plain device copy of `bytes` (multiple of 16) used to calibrate hardware
  * traffic counters against a kernel of known size.                          */

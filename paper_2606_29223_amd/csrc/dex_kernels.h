@@ -19,6 +19,22 @@ __device__ __forceinline__ int qkv_col(int tile, int r16, int hd) {
 
 typedef uint16_t bf16;
 
+// Sampling-mode Gumbel noise of token v for the slot of sequence `seq` at
+// position `pos` (the definition is stated with dex_debug_gumbel in dex.h).
+__device__ __forceinline__ unsigned long long sm64_mix(unsigned long long z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+__device__ __forceinline__ unsigned long long gumbel_key(unsigned long long seed, int seq, int pos) {
+  return sm64_mix(seed ^ sm64_mix(((unsigned long long)(unsigned)seq << 32) + (unsigned long long)(unsigned)pos));
+}
+__device__ __forceinline__ float gumbel_noise(unsigned long long key, int v) {
+  const unsigned long long z = sm64_mix(key + (unsigned long long)(v + 1) * 0x9E3779B97F4A7C15ull);
+  const float u = ((float)(unsigned)(z >> 41) + 0.5f) * (1.0f / 8388608.0f);
+  return -logf(-logf(u));
+}
+
 // ---------------------------------------------------------------- epilogues
 enum Epi {
   EPI_PLAIN = 0,   // y[m][n] (float)
@@ -78,6 +94,8 @@ struct GemmArgs {
   float *logits_tap;          // nullable [M][N]
   float2 *amax;               // [M][n_tiles] (value, index as float bits)
   int n_tiles;
+  float temperature;          // > 0: Gumbel-max sampling with the rows of (sample_seed, row_seq, row_pos)
+  unsigned long long sample_seed;
 };
 
 struct AttnArgs {
@@ -186,6 +204,7 @@ struct CollapseArgs {
 };
 hipError_t launch_collapse(const CollapseArgs &a, hipStream_t s);
 
+hipError_t launch_gumbel(unsigned long long seed, int seq, int pos, int V, float *out, hipStream_t s);
 hipError_t launch_copy(void *dst, const void *src, int64_t bytes, hipStream_t s);
 
 }  // namespace dex

@@ -81,6 +81,8 @@ struct dex_ctx {
   // config
   std::vector<int> X;
   int N, W, decs, B, max_ctx;
+  float temperature = 0.f;               // > 0: sampling mode
+  unsigned long long sample_seed = 0;
   hipStream_t stream;
   // stage lanes: lane 0 is `stream`, the others library-owned streams
   int n_lanes = 1;
@@ -373,7 +375,8 @@ dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_la
 
 // exit head over M rows whose final state sits in (src_h, src_part)[row_src[m]]
 dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h, const float *src_part,
-                    const int *mask_n, const int *mask_tok, const int *cand_idx, int *cand) {
+                    const int *mask_n, const int *mask_tok, const int *cand_idx, int *cand, const int *row_seq,
+                    const int *row_pos) {
   const hipStream_t st = ctx->stream;
   {
     PrepArgs p{};
@@ -391,6 +394,7 @@ dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h,
     a.part = ctx->ex_part; a.n_part = ctx->n_part; a.inv_d = 1.0f / ctx->d; a.eps = ctx->eps;
     a.mask_n = mask_n; a.mask_tok = mask_tok; a.mask_stride = ctx->N;
     a.logits_tap = ctx->logits_tap; a.amax = ctx->amax; a.n_tiles = n_tiles;
+    a.temperature = ctx->temperature; a.sample_seed = ctx->sample_seed; a.row_seq = row_seq; a.row_pos = row_pos;
     TimedLaunch tl(ctx, 6, wbytes(ctx, (double)ctx->V * ctx->d + (double)M * ctx->d));
     HIPCHK(launch_gemm(ctx->dtype, EPI_LOGITS, a, 1, st));
   }
@@ -465,6 +469,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   if (c->batch < 1 || c->batch > DEX_MAX_BATCH) return bad("batch out of range");
   if (c->width_cap < 0) return bad("width_cap must be >= 0");
   if (c->max_context < 2) return bad("max_context must be >= 2");
+  if (!(c->temperature >= 0.f) || !std::isfinite(c->temperature)) return bad("temperature must be finite and >= 0");
   if ((c->max_context + ATT_SPLIT - 1) / ATT_SPLIT > ATT_MAX_SPLITS) return bad("max_context too long");
   const int N = c->n_explored;
   long long per_seq = c->width_cap > 0 ? c->width_cap : (N - 1 >= 20 ? (1LL << 20) : (1LL << (N - 1)));
@@ -480,6 +485,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   ctx->X.assign(c->explored, c->explored + N);
   ctx->N = N; ctx->W = c->width_cap; ctx->decs = c->decs ? 1 : 0; ctx->B = c->batch;
   ctx->max_ctx = c->max_context; ctx->stream = (hipStream_t)c->hip_stream;
+  ctx->temperature = c->temperature; ctx->sample_seed = c->sample_seed;
   int prev = 0;
   for (int k = 0; k < N; ++k) {
     std::vector<int> ls;
@@ -649,7 +655,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
   A(&act, M * ctx->F * es);
   if (!mfma_prefill) A((void **)&apart, chunk * per_row);
   const size_t n_groups_total = (size_t)B * ((P + grp_rows - 1) / grp_rows);
-  const size_t tab_ints = M * 8 + n_groups_total * 4 + 4 * B + 64;
+  const size_t tab_ints = M * 8 + n_groups_total * 4 + 6 * B + 64;
   A((void **)&tab, tab_ints * 4);
   auto cleanup = [&]() {
     dfree(ctx, h); dfree(ctx, part); dfree(ctx, xb); dfree(ctx, q); dfree(ctx, att); dfree(ctx, act);
@@ -664,6 +670,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
   int *g_row0 = t_zero + M, *g_nrows = g_row0 + n_groups_total, *g_seq = g_nrows + n_groups_total;
   int *g_rel = g_seq + n_groups_total;
   int *ex_src = g_rel + n_groups_total, *ex_zero = ex_src + B, *ex_cidx = ex_zero + B;
+  int *ex_seq = ex_cidx + B, *ex_pos = ex_seq + B;
   for (int s = 0; s < B; ++s)
     for (int p = 0; p < P; ++p) {
       const size_t r = (size_t)s * P + p;
@@ -691,13 +698,16 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     chunks.push_back({g, e - g, c0, rows_in});
     g = e;
   }
-  for (int s = 0; s < B; ++s) { ex_src[s] = s * P + P - 1; ex_zero[s] = 0; ex_cidx[s] = 0; }
+  for (int s = 0; s < B; ++s) {
+    ex_src[s] = s * P + P - 1; ex_zero[s] = 0; ex_cidx[s] = 0; ex_seq[s] = s; ex_pos[s] = P - 1;
+  }
   HIPCHK(hipMemcpyAsync(tab, host.data(), tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
   const int *d_seq = tab, *d_pos = tab + M, *d_entry = d_pos + M, *d_tok = d_entry + M, *d_nc = d_tok + M,
             *d_coff = d_nc + M, *d_zero = d_coff + 2 * M;
   const int *d_g0 = d_zero + M, *d_gn = d_g0 + n_groups_total, *d_gs = d_gn + n_groups_total;
   const int *d_grel = d_gs + n_groups_total;
   const int *d_exsrc = d_grel + n_groups_total, *d_exzero = d_exsrc + B;
+  const int *d_exseq = d_exzero + 2 * B, *d_expos = d_exseq + B;
 
   {
     PrepArgs p{};
@@ -772,7 +782,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     }
   }
   // y_0: final-depth exit head at the last prompt position of every sequence
-  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr);
+  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr, d_exseq, d_expos);
   if (es2 != DEX_OK) { cleanup(); return fail(ctx, es2); }
   HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, B * 4, hipMemcpyDeviceToHost, ctx->stream));
   HIPCHK(hipStreamSynchronize(ctx->stream));
@@ -970,7 +980,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   }
   // ---------------------------------------------------- exit + commit
   dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),
-                           dptr(t_cidx), ctx->cand);
+                           dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos));
   if (xs != DEX_OK) return fail(ctx, xs);
   {
     CommitArgs c{};
@@ -1223,6 +1233,12 @@ dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, co
     e = M > 64 ? launch_gemm_tiled(EPI_PLAIN, a, (hipStream_t)stream) : launch_gemm(dtype, EPI_PLAIN, a, 1, (hipStream_t)stream);
   if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
   (void)hipFree(wp);
+  return e == hipSuccess ? DEX_OK : DEX_E_HIP;
+}
+
+dex_status dex_debug_gumbel(uint64_t seed, int32_t seq, int32_t pos, int32_t V, float *out, void *stream) {
+  if (!out || V < 1 || seq < 0 || pos < 0) return DEX_E_INVAL;
+  hipError_t e = launch_gumbel(seed, seq, pos, V, out, (hipStream_t)stream);
   return e == hipSuccess ? DEX_OK : DEX_E_HIP;
 }
 

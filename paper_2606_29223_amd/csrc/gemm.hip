@@ -19,8 +19,9 @@
 //   RESID   h += alpha * acc, the next RMSNorm's input g*h in the matrix-core
 //           type, and per-16-column sum-of-squares partials of h;
 //   SWIGLU  SiLU(r*gate) * (r*up) for the interleaved gate/up tiles;
-//   LOGITS  r*acc, optional float logits tap, DECS mask (-inf), and the
-//           tile's argmax (lowest id on ties);
+//   LOGITS  r*acc, optional float logits tap, in sampling mode acc/tau plus
+//           the slot's Gumbel noise, DECS mask (-inf), and the tile's argmax
+//           (lowest id on ties);
 //   PLAIN   float output (tests).
 #include "dex_kernels.h"
 
@@ -269,6 +270,9 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       float v = val[0][nl][ml] * r;
       if (n < a.N) {
         if (a.logits_tap != nullptr) a.logits_tap[(size_t)m * a.N + n] = v;
+        // sampling mode (Algorithm 2): the Gumbel row of the row's slot
+        if (a.temperature > 0.f)
+          v = v / a.temperature + gumbel_noise(gumbel_key(a.sample_seed, a.row_seq[m], a.row_pos[m]), n);
         const int nm = a.mask_n[m];
         for (int q = 0; q < nm; ++q)
           if (a.mask_tok[(size_t)m * a.mask_stride + q] == n) v = -INFINITY;

@@ -167,6 +167,17 @@ __global__ __launch_bounds__(256) void copy_kernel(uint4 *dst, const uint4 *src,
     dst[i] = src[i];
 }
 
+__global__ __launch_bounds__(256) void gumbel_kernel(unsigned long long seed, int seq, int pos, int V, float *out) {
+  const int v = blockIdx.x * 256 + threadIdx.x;
+  if (v < V) out[v] = gumbel_noise(gumbel_key(seed, seq, pos), v);
+}
+
+hipError_t launch_gumbel(unsigned long long seed, int seq, int pos, int V, float *out, hipStream_t s) {
+  if (V <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gumbel_kernel, dim3((V + 255) / 256), dim3(256), 0, s, seed, seq, pos, V, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_copy(void *dst, const void *src, int64_t bytes, hipStream_t s) {
   const int64_t n = bytes / 16;
   if (n <= 0) return hipSuccess;

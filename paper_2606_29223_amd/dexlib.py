@@ -24,7 +24,7 @@ EXPORTED = (
     "dex_create", "dex_prefill", "dex_step", "dex_destroy", "dex_last_error",
     "dex_debug_set_logits_tap", "dex_debug_lattice", "dex_debug_last_collapse",
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
-    "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_copy",
+    "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_gumbel", "dex_debug_copy",
 )
 
 
@@ -45,7 +45,8 @@ class DexConfig(ctypes.Structure):
         ("explored", ctypes.POINTER(ctypes.c_int32)), ("n_explored", ctypes.c_int32),
         ("width_cap", ctypes.c_int32), ("decs", ctypes.c_int32), ("batch", ctypes.c_int32),
         ("max_context", ctypes.c_int32), ("hip_stream", ctypes.c_void_p),
-        ("stage_streams", ctypes.c_int32),
+        ("stage_streams", ctypes.c_int32), ("temperature", ctypes.c_float),
+        ("sample_seed", ctypes.c_uint64),
     ]
 
 
@@ -97,6 +98,7 @@ def load(path: str | None = None):
     lib.dex_debug_time_kernel.argtypes = [vp, i32, i32, i32, P(ctypes.c_double), P(ctypes.c_double)]
     lib.dex_debug_gemm.argtypes = [i32, vp, i32, i32, vp, i32, vp, vp]
     lib.dex_debug_copy.argtypes = [vp, vp, i64, vp]
+    lib.dex_debug_gumbel.argtypes = [ctypes.c_uint64, i32, i32, i32, vp, vp]
     for name in EXPORTED:
         if name not in ("dex_destroy", "dex_last_error"):
             getattr(lib, name).restype = ctypes.c_int32
@@ -169,7 +171,7 @@ class Decoder:
     """One library context over device-resident weights."""
 
     def __init__(self, cfg: dict, dev_weights: dict, explored=None, width_cap=None, decs=None,
-                 batch=None, max_context=None, stream=None, stage_streams=0):
+                 batch=None, max_context=None, stream=None, stage_streams=0, temperature=0.0, seed=0):
         import torch
         self.lib = load()
         self.cfg = cfg
@@ -203,6 +205,8 @@ class Decoder:
         self.stream = stream if stream is not None else torch.cuda.Stream()
         c.hip_stream = self.stream.cuda_stream
         c.stage_streams = int(stage_streams)
+        c.temperature = float(temperature)
+        c.sample_seed = int(seed) & ((1 << 64) - 1)
         torch.cuda.synchronize()                # weights uploaded on other streams are complete
         self.model_struct, self.config_struct = m, c
         self.max_context = c.max_context

@@ -78,9 +78,20 @@ def test_create_rejects_bad_dims(lib):
         assert lib.dex_create(ctypes.byref(m), ctypes.byref(c), ctypes.byref(ctx)) == dexlib.DEX_E_INVAL
 
 
+@pytest.mark.parametrize("tau", [-0.5, float("nan"), float("inf")])
+def test_create_rejects_bad_temperature(lib, tau):
+    m, _a, _f = _model()
+    c, _x = _config([4])
+    c.temperature = tau
+    ctx = ctypes.c_void_p()
+    assert lib.dex_create(ctypes.byref(m), ctypes.byref(c), ctypes.byref(ctx)) == dexlib.DEX_E_INVAL
+    assert "temperature" in lib.dex_last_error(None).decode()
+
+
 def test_null_and_state_errors(lib):
     assert lib.dex_step(None, None, None) == dexlib.DEX_E_INVAL
     assert lib.dex_prefill(None, None, 0, None) == dexlib.DEX_E_INVAL
     lib.dex_destroy(None)
     assert lib.dex_debug_copy(None, None, 16, None) == dexlib.DEX_E_INVAL
     assert lib.dex_debug_gemm(1, None, 16, 16, None, 1, None, None) == dexlib.DEX_E_INVAL
+    assert lib.dex_debug_gumbel(1, 0, 0, 16, None, None) == dexlib.DEX_E_INVAL
