@@ -7,10 +7,11 @@ with the GPU library; both read the same seeded inputs from synth/.
 Modules: model (the synthetic decoder and exit heads), ar (AR decoding and
 teacher-forced exit logits), lattice (Algorithm 1 / Section 3.2 bookkeeping
 with Algorithm 2's masks), dex (the full procedure on the model), gumbel
-(Algorithm 2's sampling-mode noise and decode rule), ead (Section 2's
-accounting, used as test pins).
+(Algorithm 2's sampling-mode noise and decode rule), adapter (the inducing
+adapter of non-final depths), ead (Section 2's accounting, used as test
+pins).
 """
-from . import ar, dex, ead, gumbel, lattice, model  # noqa: F401
+from . import adapter, ar, dex, ead, gumbel, lattice, model  # noqa: F401
 from .model import Model  # noqa: F401
 
 

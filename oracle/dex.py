@@ -21,6 +21,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
+from . import adapter as adapter_mod
 from .ar import Cache
 from .gumbel import decode
 from .lattice import Lattice
@@ -67,12 +68,14 @@ def validate_explored(explored, L):
 
 def dex_generate(model: Model, prompt, explored, width_cap: int, decs: bool, T: int,
                  max_context: int | None = None, force=None, prefill=None, keep_trace=True,
-                 check=None, temperature: float = 0.0, seed: int = 0, seq: int = 0):
+                 check=None, temperature: float = 0.0, seed: int = 0, seq: int = 0, adapters=None):
     """Run DEX until T tokens are generated (y_0 from the prefill included).
 
     temperature > 0 selects Algorithm 2's sampling mode: every node decodes
     argmax(l / temperature + G) with the Gumbel row of (seed, seq, its
     position) (oracle/gumbel.py); 0 is greedy.
+    adapters: None, or one inducing adapter per non-final stage (dicts of
+    oracle/adapter.PARTS); a node at stage k < N-1 decodes h + dh_k(h).
 
     force(prefix_tokens, stage, natural_token, mask) may return a token that
     replaces a node's candidate (used by the brute-force test to steer the
@@ -108,7 +111,10 @@ def dex_generate(model: Model, prompt, explored, width_cap: int, decs: bool, T: 
                 s.state.setdefault("k", {})[l] = kk
                 s.state.setdefault("v", {})[l] = vv
             s.state["h"] = h
-            z = model.exit_logits(h)
+            if adapters is not None and k < N - 1:
+                z = model.exit_logits(h + adapter_mod.delta(adapters[k], h, model.eps))
+            else:
+                z = model.exit_logits(h)
             m = lat.mask(s, k)
             tok = decode(z, m, temperature, seed, seq, s.pos)
             if force is not None:

@@ -201,6 +201,54 @@ def generate_model(cfg: dict, force_numpy: bool = False) -> dict:
     return out
 
 
+def adapter_specs(cfg: dict):
+    """[(name, shape, kind)] of the inducing adapters, one per non-final
+    explored depth (index k of the explored list), hidden width m = 2d."""
+    d = cfg["d_model"]
+    m = 2 * d
+    specs = []
+    for k in range(len(cfg["explored"]) - 1):
+        specs += [
+            (f"adapters.{k}.norm", (d,), "gain"),
+            (f"adapters.{k}.w1", (m, d), "matrix"),
+            (f"adapters.{k}.b1", (m,), "bias"),
+            (f"adapters.{k}.w2", (d, m), "matrix"),
+            (f"adapters.{k}.b2", (d,), "bias"),
+        ]
+    return specs
+
+
+def generate_adapters(cfg: dict, alpha: float, force_numpy: bool = False) -> dict:
+    """Synthetic inducing adapters (the paper trains them; these stand in):
+    matrices uniform with variance 1/in (bf16 bits for bf16 models), norm
+    gains 1 + 0.05 * uniform(-1, 1), biases uniform(-0.1, 0.1) float32, and
+    the gate alpha (float32 [1]) set to `alpha` at every depth."""
+    bf16 = cfg["dtype"] == "bf16"
+    out = {}
+    base = mix64((cfg["model_seed"] + 0xADA97E) & _MASK)
+    for idx, (name, shape, kind) in enumerate(adapter_specs(cfg)):
+        key = mix64((base + idx) & _MASK)
+        n = int(np.prod(shape))
+        if kind == "gain":
+            arr = uniform(key, n, 0.05, 1.0, bf16=False, force_numpy=force_numpy)
+        elif kind == "bias":
+            arr = uniform(key, n, 0.1, 0.0, bf16=False, force_numpy=force_numpy)
+        else:
+            a = math.sqrt(3.0 / shape[1])
+            arr = uniform(key, n, a, 0.0, bf16=bf16, force_numpy=force_numpy)
+        out[name] = arr.reshape(shape)
+    for k in range(len(cfg["explored"]) - 1):
+        out[f"adapters.{k}.alpha"] = np.array([alpha], dtype=np.float32)
+    return out
+
+
+def adapters_as_f64(cfg: dict, ad: dict) -> list:
+    """Per non-final depth, the adapter tensors as exact binary64 (oracle)."""
+    f = model_as_f64(cfg, ad)
+    return [{p: f[f"adapters.{k}.{p}"] for p in ("norm", "w1", "b1", "w2", "b2", "alpha")}
+            for k in range(len(cfg["explored"]) - 1)]
+
+
 def prompts(cfg: dict, force_numpy: bool = False) -> np.ndarray:
     """int32 [batch, prompt_len], uniform over the vocabulary."""
     rows = []
