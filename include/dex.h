@@ -118,6 +118,16 @@ typedef struct {
                                            sequence, position of the node's input token)
                                            (see dex_debug_gumbel below) */
   uint64_t sample_seed;
+  int32_t adapter_dim;                  /* 0: no adapters.  Else m, the hidden width of the
+                                           inducing adapters (Section 3.4 and its appendix):
+                                           a node at a non-final explored depth k decodes
+                                           h + dh_k(h), dh = alpha (W2 silu(W1 RMSNorm(h; g)
+                                           + b1) + b2); the final depth is never adapted */
+  const void *const *adapters;          /* [n_explored - 1][6] device pointers per non-final
+                                           depth: g float[d], W1 [m][d], b1 float[m],
+                                           W2 [d][m], b2 float[d], alpha float[1]; matrices in
+                                           weight_dtype.  Borrowed: read at create (the
+                                           library keeps repacked copies and alpha) */
 } dex_config;
 
 /* What one dex_step did (all host memory).  Rows are listed stage-major,

@@ -62,10 +62,13 @@ def ar_generate(model: Model, prompt, T: int, prefill=None, temperature: float =
     return toks
 
 
-def depth_logits(model: Model, prompt, seq, depths, prefill=None):
+def depth_logits(model: Model, prompt, seq, depths, prefill=None, adapters=None):
     """Teacher-forced exit logits.  For t = 1..len(seq)-1 the row at position
     P+t-1 has input seq[t-1] and prefix prompt || seq[:t-1]; returns an array
-    [len(seq)-1, len(depths), V] of z_d for d in `depths` (1-based)."""
+    [len(seq)-1, len(depths), V] of z_d for d in `depths` (1-based).
+    adapters: None, or the inducing adapters of depths[:-1] (decoded as
+    h + dh, oracle/adapter.py)."""
+    from .adapter import delta
     P = len(prompt)
     Ks, Vs, _ = prefill if prefill is not None else model.prefill(prompt)
     cache = Cache(model, Ks, Vs, P + len(seq))
@@ -74,7 +77,10 @@ def depth_logits(model: Model, prompt, seq, depths, prefill=None):
         pos = P + t - 1
         hs = decode_row(model, cache, seq[t - 1], pos)
         for j, d in enumerate(depths):
-            out[t - 1, j] = model.exit_logits(hs[d - 1])
+            h = hs[d - 1]
+            if adapters is not None and j < len(depths) - 1:
+                h = h + delta(adapters[j], h, model.eps)
+            out[t - 1, j] = model.exit_logits(h)
     return out
 
 

@@ -42,6 +42,7 @@ enum Epi {
   EPI_RESID = 2,   // h += alpha * y; next-norm input and sum-of-squares partials
   EPI_SWIGLU = 3,  // rms-scaled gate/up pair -> SiLU(gate) * up
   EPI_LOGITS = 4,  // rms-scaled LM head, DECS mask, per-tile argmax
+  EPI_BIAS_SILU = 5,  // SiLU(rms-scaled y + bias) -> act (adapter up-projection)
 };
 
 constexpr int GEMM_WAVES = 8;       // split-K ways inside a workgroup
@@ -84,6 +85,7 @@ struct GemmArgs {
   int n_part_out;
   const int *row_bnd;         // nullable: write h/partials to boundary storage instead
   float *bnd_h, *bnd_part;
+  const float *bias;          // RESID (nullable): h += alpha * (y + bias); BIAS_SILU: SiLU(y + bias)
   // SWIGLU
   void *act;                  // [M][ld_act] (T)
   int ld_act;

@@ -96,6 +96,13 @@ struct dex_ctx {
   std::vector<void *> p_qkv, p_o, p_gu, p_down;
   void *p_lm = nullptr;
   int ns_d = 0, ns_hhd = 0, ns_F = 0;
+  // inducing adapters of the non-final depths: packed W1 [m][d] and W2 [d][m]
+  // (library-owned), borrowed norm gains and biases, the gates on the host
+  int ad_m = 0, ns_m = 0;
+  std::vector<void *> p_ad1, p_ad2;
+  std::vector<const float *> ad_norm, ad_b1, ad_b2;
+  std::vector<float> ad_alpha;
+  void *ad_act = nullptr;                 // [R][m] (T)
   // device buffers
   void *kc = nullptr, *vc = nullptr;
   float2 *rope = nullptr;
@@ -374,17 +381,70 @@ dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_la
 }
 
 // exit head over M rows whose final state sits in (src_h, src_part)[row_src[m]]
+// Rows [r0, r0 + M) of the exit buffers from their source states, with the
+// next norm's input g * h.
+dex_status exit_prep(dex_ctx *ctx, int r0, int M, const int *row_src, const float *src_h, const float *src_part,
+                     const float *g) {
+  if (M <= 0) return DEX_OK;
+  PrepArgs p{};
+  p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = 0;
+  p.row_src = row_src + r0; p.bnd_h = src_h; p.bnd_part = src_part; p.g = g;
+  p.h = ctx->ex_h + (size_t)r0 * ctx->d; p.part = ctx->ex_part + (size_t)r0 * ctx->n_part;
+  p.xb = (char *)ctx->ex_xb + (size_t)r0 * ctx->d * ctx->es;
+  TimedLaunch tl(ctx, 7, 0.0);
+  HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
+  return DEX_OK;
+}
+
+// Inducing adapter of non-final depth k on exit rows [r0, r0 + M), whose
+// states and g_k * h are in the exit buffers: h <- h + alpha (W2 silu(W1
+// RMSNorm(h; g_k) + b1) + b2), then the final norm's input and partials.
+dex_status exit_adapter(dex_ctx *ctx, int k, int r0, int M) {
+  if (M <= 0) return DEX_OK;
+  const int d = ctx->d, m = ctx->ad_m;
+  void *xb = (char *)ctx->ex_xb + (size_t)r0 * d * ctx->es;
+  float *part = ctx->ex_part + (size_t)r0 * ctx->n_part;
+  void *act = (char *)ctx->ad_act + (size_t)r0 * m * ctx->es;
+  {
+    GemmArgs a{};
+    a.wp = ctx->p_ad1[k]; a.nsteps_w = ctx->ns_d; a.N = m; a.K = d;
+    a.x = xb; a.ldx = d; a.M = M; a.part = part; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+    a.act = act; a.ld_act = m; a.bias = ctx->ad_b1[k];
+    TimedLaunch tl(ctx, 7, 0.0);
+    HIPCHK(launch_gemm(ctx->dtype, EPI_BIAS_SILU, a, 1, ctx->stream));
+  }
+  {
+    GemmArgs a{};
+    a.wp = ctx->p_ad2[k]; a.nsteps_w = ctx->ns_m; a.N = d; a.K = m;
+    a.x = act; a.ldx = m; a.M = M;
+    a.h = ctx->ex_h + (size_t)r0 * d; a.ld_h = d; a.alpha = ctx->ad_alpha[k]; a.bias = ctx->ad_b2[k];
+    a.g_next = ctx->final_norm; a.xb = xb; a.part_out = part; a.n_part_out = ctx->n_part;
+    TimedLaunch tl(ctx, 7, 0.0);
+    HIPCHK(launch_gemm(ctx->dtype, EPI_RESID, a, 1, ctx->stream));
+  }
+  return DEX_OK;
+}
+
+// exit head over M rows whose final state sits in (src_h, src_part)[row_src[m]];
+// stage_r0 (host, N + 1 bounds of the stage-major rows) selects the rows of
+// non-final depths for the adapters (nullptr: every row is final depth)
 dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h, const float *src_part,
                     const int *mask_n, const int *mask_tok, const int *cand_idx, int *cand, const int *row_seq,
-                    const int *row_pos) {
+                    const int *row_pos, const int *stage_r0) {
   const hipStream_t st = ctx->stream;
-  {
-    PrepArgs p{};
-    p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = 0;
-    p.row_src = row_src; p.bnd_h = src_h; p.bnd_part = src_part; p.g = ctx->final_norm;
-    p.h = ctx->ex_h; p.part = ctx->ex_part; p.xb = ctx->ex_xb;
-    TimedLaunch tl(ctx, 7, 0.0);
-    HIPCHK(launch_prep(ctx->dtype, p, st));
+  if (ctx->ad_m > 0 && stage_r0 != nullptr) {
+    const int N = ctx->N;
+    for (int k = 0; k + 1 < N; ++k) {
+      const int b0 = stage_r0[k], nb = stage_r0[k + 1] - b0;
+      dex_status s1 = exit_prep(ctx, b0, nb, row_src, src_h, src_part, ctx->ad_norm[k]);
+      if (s1 == DEX_OK) s1 = exit_adapter(ctx, k, b0, nb);
+      if (s1 != DEX_OK) return s1;
+    }
+    dex_status s2 = exit_prep(ctx, stage_r0[N - 1], M - stage_r0[N - 1], row_src, src_h, src_part, ctx->final_norm);
+    if (s2 != DEX_OK) return s2;
+  } else {
+    dex_status s2 = exit_prep(ctx, 0, M, row_src, src_h, src_part, ctx->final_norm);
+    if (s2 != DEX_OK) return s2;
   }
   const int n_tiles = (ctx->V + 15) / 16;
   {
@@ -470,6 +530,13 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   if (c->width_cap < 0) return bad("width_cap must be >= 0");
   if (c->max_context < 2) return bad("max_context must be >= 2");
   if (!(c->temperature >= 0.f) || !std::isfinite(c->temperature)) return bad("temperature must be finite and >= 0");
+  if (c->adapter_dim < 0) return bad("adapter_dim must be >= 0");
+  if (c->adapter_dim > 0) {
+    if (c->adapter_dim % epb) return bad("adapter_dim must be a multiple of 8 (bf16) / 4 (f32)");
+    if (!c->adapters) return bad("adapter_dim > 0 needs the adapter pointers");
+    for (int i = 0; i < (c->n_explored - 1) * 6; ++i)
+      if (!c->adapters[i]) return bad("null adapter pointer");
+  }
   if ((c->max_context + ATT_SPLIT - 1) / ATT_SPLIT > ATT_MAX_SPLITS) return bad("max_context too long");
   const int N = c->n_explored;
   long long per_seq = c->width_cap > 0 ? c->width_cap : (N - 1 >= 20 ? (1LL << 20) : (1LL << (N - 1)));
@@ -523,6 +590,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   A((void **)&ctx->ex_h, R * d * 4);
   A((void **)&ctx->ex_part, R * ctx->n_part * 4);
   A(&ctx->ex_xb, R * d * es);
+  if (c->adapter_dim > 0) A(&ctx->ad_act, R * (size_t)c->adapter_dim * es);
   A((void **)&ctx->amax, R * ((ctx->V + 15) / 16) * sizeof(float2));
   A((void **)&ctx->u_dev, R * 4 + 256);
   A((void **)&ctx->commit_dev, (size_t)ctx->B * 2 * 4 + 256);
@@ -589,6 +657,26 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       if (ps == DEX_OK) ps = pack(&ctx->p_down[l], LW(ctx, l, DEX_P_W_DOWN), nullptr, nullptr, dd, 0, 0, dd, F, 0);
     }
     if (ps == DEX_OK) ps = pack(&ctx->p_lm, ctx->lm_head, nullptr, nullptr, ctx->V, 0, 0, ctx->V, dd, 0);
+    if (ps == DEX_OK && c->adapter_dim > 0) {
+      const int am = c->adapter_dim;
+      ctx->ad_m = am;
+      ctx->ns_m = (am + kstep - 1) / kstep;
+      ctx->p_ad1.assign(N - 1, nullptr); ctx->p_ad2.assign(N - 1, nullptr);
+      ctx->ad_norm.assign(N - 1, nullptr); ctx->ad_b1.assign(N - 1, nullptr); ctx->ad_b2.assign(N - 1, nullptr);
+      ctx->ad_alpha.assign(N - 1, 0.f);
+      for (int k = 0; k + 1 < N && ps == DEX_OK; ++k) {
+        const void *const *ap = c->adapters + (size_t)k * 6;
+        ctx->ad_norm[k] = (const float *)ap[0];
+        ctx->ad_b1[k] = (const float *)ap[2];
+        ctx->ad_b2[k] = (const float *)ap[4];
+        ps = pack(&ctx->p_ad1[k], ap[1], nullptr, nullptr, am, 0, 0, am, dd, 0);
+        if (ps == DEX_OK) ps = pack(&ctx->p_ad2[k], ap[3], nullptr, nullptr, dd, 0, 0, dd, am, 0);
+        if (ps == DEX_OK && hipMemcpy(&ctx->ad_alpha[k], ap[5], sizeof(float), hipMemcpyDeviceToHost) != hipSuccess) {
+          ctx->err = "reading an adapter gate failed";
+          ps = DEX_E_HIP;
+        }
+      }
+    }
     if (ps == DEX_OK && hipDeviceSynchronize() != hipSuccess) { ctx->err = "weight packing failed"; ps = DEX_E_HIP; }
     if (ps != DEX_OK) {
       g_create_error = ctx->err;
@@ -782,7 +870,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     }
   }
   // y_0: final-depth exit head at the last prompt position of every sequence
-  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr, d_exseq, d_expos);
+  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr, d_exseq, d_expos, nullptr);
   if (es2 != DEX_OK) { cleanup(); return fail(ctx, es2); }
   HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, B * 4, hipMemcpyDeviceToHost, ctx->stream));
   HIPCHK(hipStreamSynchronize(ctx->stream));
@@ -980,7 +1068,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   }
   // ---------------------------------------------------- exit + commit
   dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),
-                           dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos));
+                           dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos), stage_r0.data());
   if (xs != DEX_OK) return fail(ctx, xs);
   {
     CommitArgs c{};

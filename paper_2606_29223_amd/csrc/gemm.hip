@@ -19,6 +19,8 @@
 //   RESID   h += alpha * acc, the next RMSNorm's input g*h in the matrix-core
 //           type, and per-16-column sum-of-squares partials of h;
 //   SWIGLU  SiLU(r*gate) * (r*up) for the interleaved gate/up tiles;
+//   BIAS_SILU  SiLU(r*acc + bias) (the inducing adapter's first layer);
+//   RESID with a bias: h += alpha * (acc + bias) (its second layer);
 //   LOGITS  r*acc, optional float logits tap, in sampling mode acc/tau plus
 //           the slot's Gumbel noise, DECS mask (-inf), and the tile's argmax
 //           (lowest id on ties);
@@ -235,7 +237,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int m = m0 + ml, n = tile * 16 + nl;
       const float *hin = a.h + (size_t)m * a.ld_h;
       float *hout = (a.row_bnd != nullptr) ? a.bnd_h + (size_t)a.row_bnd[m] * a.ld_h : a.h + (size_t)m * a.ld_h;
-      const float br = a.alpha * val[0][nl][ml];
+      const float br = (a.bias != nullptr) ? a.alpha * (val[0][nl][ml] + a.bias[n]) : a.alpha * val[0][nl][ml];
       const float hn = hin[n] + br;
       hout[n] = hn;
       if (a.xb != nullptr) ((T *)a.xb)[(size_t)m * a.ld_h + n] = to_t<T>(a.g_next[n] * hn);
@@ -260,6 +262,15 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const float gt = val[0][nl][ml] * r, up = val[NT - 1][nl][ml] * r;
       const float sg = gt / (1.0f + expf(-gt));
       ((T *)a.act)[(size_t)m * a.ld_act + n] = to_t<T>(sg * up);
+    }
+  } else if constexpr (EPI == EPI_BIAS_SILU) {
+    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
+      const int ml = e / 16, nl = e % 16;
+      const int m = m0 + ml, n = tile * 16 + nl;
+      if (n >= a.N) continue;
+      const float r = (a.part != nullptr) ? rs[ml] : 1.f;
+      const float u = val[0][nl][ml] * r + a.bias[n];
+      ((T *)a.act)[(size_t)m * a.ld_act + n] = to_t<T>(u / (1.0f + expf(-u)));
     }
   } else if constexpr (EPI == EPI_LOGITS) {
     __shared__ float z[16][16 * MB];
@@ -364,6 +375,7 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipS
       case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, m_blocks, s);
       case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, m_blocks, s);
       case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, m_blocks, s);
+      case EPI_BIAS_SILU: return launch_t<bf16, EPI_BIAS_SILU>(a, m_blocks, s);
     }
   } else {
     switch (epi) {
@@ -372,6 +384,7 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipS
       case EPI_RESID: return launch_t<float, EPI_RESID>(a, m_blocks, s);
       case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, m_blocks, s);
       case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, m_blocks, s);
+      case EPI_BIAS_SILU: return launch_t<float, EPI_BIAS_SILU>(a, m_blocks, s);
     }
   }
   return hipErrorInvalidValue;

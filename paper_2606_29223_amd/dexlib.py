@@ -19,6 +19,7 @@ DEX_OK, DEX_E_INVAL, DEX_E_NOMEM, DEX_E_HIP, DEX_E_STATE, DEX_E_CAPACITY = 0, -1
 DEX_F32, DEX_BF16 = 0, 1
 DEX_MAX_BATCH, DEX_MAX_EXPLORED, DEX_MAX_ROWS = 64, 32, 256
 LAYER_PARAMS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+ADAPTER_PARTS = ("norm", "w1", "b1", "w2", "b2", "alpha")
 
 EXPORTED = (
     "dex_create", "dex_prefill", "dex_step", "dex_destroy", "dex_last_error",
@@ -46,7 +47,8 @@ class DexConfig(ctypes.Structure):
         ("width_cap", ctypes.c_int32), ("decs", ctypes.c_int32), ("batch", ctypes.c_int32),
         ("max_context", ctypes.c_int32), ("hip_stream", ctypes.c_void_p),
         ("stage_streams", ctypes.c_int32), ("temperature", ctypes.c_float),
-        ("sample_seed", ctypes.c_uint64),
+        ("sample_seed", ctypes.c_uint64), ("adapter_dim", ctypes.c_int32),
+        ("adapters", ctypes.POINTER(ctypes.c_void_p)),
     ]
 
 
@@ -171,7 +173,8 @@ class Decoder:
     """One library context over device-resident weights."""
 
     def __init__(self, cfg: dict, dev_weights: dict, explored=None, width_cap=None, decs=None,
-                 batch=None, max_context=None, stream=None, stage_streams=0, temperature=0.0, seed=0):
+                 batch=None, max_context=None, stream=None, stage_streams=0, temperature=0.0, seed=0,
+                 adapters=None):
         import torch
         self.lib = load()
         self.cfg = cfg
@@ -207,6 +210,15 @@ class Decoder:
         c.stage_streams = int(stage_streams)
         c.temperature = float(temperature)
         c.sample_seed = int(seed) & ((1 << 64) - 1)
+        # inducing adapters: device tensors "adapters.{k}.{part}" for the
+        # non-final explored depths k (see ADAPTER_PARTS)
+        self.adapters = adapters
+        if adapters is not None:
+            n_ad = self.N - 1
+            ptrs = [adapters[f"adapters.{k}.{p}"].data_ptr() for k in range(n_ad) for p in ADAPTER_PARTS]
+            self._adp = (ctypes.c_void_p * max(len(ptrs), 1))(*ptrs)
+            c.adapters = ctypes.cast(self._adp, ctypes.POINTER(ctypes.c_void_p))
+            c.adapter_dim = int(adapters["adapters.0.w1"].shape[0]) if n_ad > 0 else 0
         torch.cuda.synchronize()                # weights uploaded on other streams are complete
         self.model_struct, self.config_struct = m, c
         self.max_context = c.max_context
