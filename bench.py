@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--temperature", type=float, default=0.0,
                    help="> 0: Algorithm 2's sampling mode (Gumbel-max, seed --seed); 0: greedy")
     p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--adapter-alpha", type=float, default=None,
+                   help="attach synthetic inducing adapters with this gate to the non-final depths")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     return p.parse_args()
 
@@ -113,7 +115,11 @@ def main():
         max_ctx = P + need
 
     samp = dict(temperature=args.temperature, seed=args.seed)
-    dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx, **samp)
+    dev_ad = None
+    if args.adapter_alpha is not None:
+        dev_ad = dexlib.device_weights(cfg, gen.generate_adapters(cfg, args.adapter_alpha))
+        torch.cuda.synchronize()
+    dec = dexlib.Decoder(cfg, dev_w, max_context=max_ctx, adapters=dev_ad, **samp)
     torch.cuda.synchronize()
     tp = time.perf_counter()
     dec.prefill(prompts)
@@ -123,6 +129,8 @@ def main():
 
     m_hist = {}
     kstar_hist = {}
+
+    ad_runs = [0]       # non-final stages with exit rows: each streams its adapter
 
     def steps(n):
         commits = rounds = layers = row_layers = 0
@@ -136,6 +144,8 @@ def main():
                 mk = dec.info.rows_per_stage[k]
                 if mk:
                     m_hist[mk] = m_hist.get(mk, 0) + 1
+                    if k < dec.N - 1:
+                        ad_runs[0] += 1
             for b in range(B):
                 ks = dec.info.kstar[b]
                 if ks >= 0:
@@ -148,6 +158,7 @@ def main():
     warm_s = time.perf_counter() - tw
     m_hist.clear()
     kstar_hist.clear()
+    ad_runs[0] = 0
     t0 = time.perf_counter()
     commits, rounds, layers, row_layers = steps(args.steps)
     torch.cuda.synchronize()
@@ -157,6 +168,7 @@ def main():
     # prefill plus every commit, over prefill and all decode rounds so far
     e2e = (B + warm_commits + commits) / (prefill_s + warm_s + elapsed)
     kstar_timed = dict(kstar_hist)
+    ad_runs_timed = ad_runs[0]
 
     # instrumented run of the same length: per-kernel HIP event durations
     # (each launch bracketed by events; includes the event overhead)
@@ -215,7 +227,8 @@ def main():
     d, F, V = cfg["d_model"], cfg["d_ffn"], cfg["vocab"]
     layer_bytes = es * (d * (cfg["n_heads"] + 2 * cfg["n_kv_heads"]) * cfg["head_dim"]
                         + cfg["n_heads"] * cfg["head_dim"] * d + 3 * d * F)
-    bytes_per_commit = (layers * layer_bytes + rounds * es * V * d) / max(commits, 1)
+    ad_bytes = (ad_runs_timed * 2 * d * (2 * d) * es) if args.adapter_alpha is not None else 0
+    bytes_per_commit = (layers * layer_bytes + rounds * es * V * d + ad_bytes) / max(commits, 1)
     hbm_bytes_per_commit = bytes_per_commit + attn_bytes_per_round * rounds / max(commits, 1)
     cpu = None
     if not args.no_cpu_baseline:
@@ -239,7 +252,9 @@ def main():
         "config": {"workload": cfg["name"], "explored": cfg["explored"], "width_cap": cfg["width_cap"],
                    "batch": B, "prompt_len": P, "parallelism": "single GPU",
                    "decoding": (f"sampling, temperature {args.temperature}, seed {args.seed}"
-                                if args.temperature > 0 else "greedy")},
+                                if args.temperature > 0 else "greedy"),
+                   "adapters": (f"synthetic, gate {args.adapter_alpha}" if args.adapter_alpha is not None
+                                else None)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "dex": {"commits": commits, "rounds": rounds, "rounds_per_commit": round(rounds / max(commits, 1), 4),
