@@ -86,13 +86,15 @@ __device__ __forceinline__ float row_rscale(const float *part, int n_part, float
   return 1.0f / sqrtf(s * inv_d + eps);
 }
 
-template <typename T, int EPI, int MB>
+// U: k-steps per prefetch chunk (two chunks in flight per wave).  It only
+// sets how far loads run ahead: every wave still accumulates its steps in
+// increasing order, so the result does not depend on U.
+template <typename T, int EPI, int MB, int U>
 __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   using F = Frag<T>;
   constexpr int EPB = F::EPB;
   constexpr int KSTEP = 4 * EPB;               // k covered by one 16-byte step of a wave
   constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;
-  constexpr int U = 4;                         // steps per prefetch chunk
   __shared__ float red[GEMM_WAVES][NT][MB][64][4];
   __shared__ float val[NT][16][16 * MB];
   __shared__ float rs[16 * MB];
@@ -358,11 +360,15 @@ static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
   dim3 block(GEMM_THREADS);
   if (m_blocks <= 0) return hipErrorInvalidValue;
   if (a.M <= 16) {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    // deeper prefetch when a workgroup per CU streams a long tile, shallower
+    // when many workgroups share each CU (measured on the 4096-wide layers)
+    if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8>), dim3(n_tiles, 1), block, 0, s, a);
+    else if (n_tiles <= 1024) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 4>), dim3(n_tiles, 1), block, 0, s, a);
+    else hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2>), dim3(n_tiles, 1), block, 0, s, a);
   } else if (a.M <= 32) {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, 2>), dim3(n_tiles, 1), block, 0, s, a);
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4>), dim3(n_tiles, 1), block, 0, s, a);
   } else {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, 4>), dim3(n_tiles, (a.M + 63) / 64), block, 0, s, a);
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4>), dim3(n_tiles, (a.M + 63) / 64), block, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -28,10 +28,10 @@ import statistics
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 SHORT = {
-    "gemm_kernel<unsigned short, 1, 1>": "qkv (bf16, M<=16)",
-    "gemm_kernel<unsigned short, 2, 1>": "o-proj / down (bf16, M<=16)",
-    "gemm_kernel<unsigned short, 3, 1>": "gate/up (bf16, M<=16)",
-    "gemm_kernel<unsigned short, 4, 1>": "lm-head (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 1, 1,": "qkv (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 2, 1,": "o-proj / down (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 3, 1,": "gate/up (bf16, M<=16)",
+    "gemm_kernel<unsigned short, 4, 1,": "lm-head (bf16, M<=16)",
 }
 
 
@@ -109,13 +109,13 @@ def traffic(args):
         copies = [v for n, v in disp if n.startswith("copy_kernel")]
         res[counter] = {"copy_kib": statistics.median(copies)}
         # the decode GEMM launches of traffic_run: (reps + 1) per class, in class order
-        seq = {"o_proj": ("gemm_kernel<unsigned short, 2, 1>", 0),
-               "down": ("gemm_kernel<unsigned short, 2, 1>", 1),
-               "gate_up": ("gemm_kernel<unsigned short, 3, 1>", 0),
-               "lm_head": ("gemm_kernel<unsigned short, 4, 1>", 0)}
+        seq = {"o_proj": ("gemm_kernel<unsigned short, 2, 1,", 0),
+               "down": ("gemm_kernel<unsigned short, 2, 1,", 1),
+               "gate_up": ("gemm_kernel<unsigned short, 3, 1,", 0),
+               "lm_head": ("gemm_kernel<unsigned short, 4, 1,", 0)}
         for cls, (name, idx) in seq.items():
             vals = [v for n, v in disp if n.startswith(name)]
-            groups = {"gemm_kernel<unsigned short, 2, 1>": 2}.get(name, 1)
+            groups = {"gemm_kernel<unsigned short, 2, 1,": 2}.get(name, 1)
             vals = vals[-groups * (reps + 1):]
             vals = vals[idx * (reps + 1) + 1:(idx + 1) * (reps + 1)]   # drop the warm-up launch
             res[counter][cls] = statistics.median(vals) if vals else None
