@@ -308,3 +308,40 @@ def test_stage_streams_do_not_change_results():
         assert a["rows"] == b["rows"] and a["kstar"] == b["kstar"] and a["collapse"] == b["collapse"]
         assert all(np.array_equal(x, y) for x, y in zip(a["lattice"], b["lattice"]))
         assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+
+
+def test_small_bf16_long_context_merged_blocks():
+    """A 2600-token prompt (41 key splits, several beyond one wave's reach of
+    64 rows' groups): DEX still equals plain AR bit for bit, and the tokens
+    and exit logits follow the float64 oracle at long context."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = configs.get(SMALL, prompt_len=2600, prompt_seeds=[9001])
+    _, w = host_weights(SMALL)
+    P, T = cfg["prompt_len"], 16
+    prompt = gen.prompts(cfg)
+    dev = device_weights(SMALL)
+    ar_dec = dexlib.Decoder(cfg, dev, explored=[cfg["n_layers"]], width_cap=1, max_context=P + T)
+    ar_toks, _ = _run(ar_dec, prompt, T, collapse=False)
+    ar_dec.close()
+    dec = dexlib.Decoder(cfg, dev, max_context=P + T)
+    tap = torch.empty((8, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    toks, rounds = _run(dec, prompt, T, tap=tap)
+    dec.close()
+    assert np.array_equal(toks, ar_toks)
+    _replay(rounds, len(cfg["explored"]), cfg["width_cap"], cfg["decs"], P + T, toks[0][0], P)
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    pl = [int(t) for t in prompt[0]]
+    pf = m.prefill(pl)
+    seq = [int(t) for t in toks[0]]
+    z = ar.depth_logits(m, pl, seq, cfg["explored"], prefill=pf)
+    check_tokens_teacher_forced(z[:, -1], seq)
+    worst, seen = 0.0, 0
+    for rd in rounds:
+        for r, (s, slot, stage, pos, tok) in enumerate(rd["rows"]):
+            if slot == 0 and pos - P < len(seq) - 1:
+                worst = max(worst, max_rel_err(rd["logits"][r], z[pos - P, stage]))
+                seen += 1
+    assert seen >= T
+    assert worst <= LOGIT_RTOL, worst
