@@ -88,25 +88,36 @@ __device__ __forceinline__ float row_rscale(const float *part, int n_part, float
 
 // U: k-steps per prefetch chunk (two chunks in flight per wave).  It only
 // sets how far loads run ahead: every wave still accumulates its steps in
-// increasing order, so the result does not depend on U.
-template <typename T, int EPI, int MB, int U>
+// increasing order, so the result does not depend on U.  NTW: weight tiles
+// per workgroup; with many rows a second tile halves the activation loads
+// per weight byte.  A tile's sums are the same per-wave partials added in
+// the same order whatever NTW is, so neither changes any result bit.
+template <typename T, int EPI, int MB, int U, int NTW>
 __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   using F = Frag<T>;
   constexpr int EPB = F::EPB;
   constexpr int KSTEP = 4 * EPB;               // k covered by one 16-byte step of a wave
   constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;
-  __shared__ float red[GEMM_WAVES][NT][MB][64][4];
-  __shared__ float val[NT][16][16 * MB];
+  constexpr int NA = NT * NTW;                 // weight blocks per step of the workgroup
+  __shared__ float red[GEMM_WAVES][NA][MB][64][4];
+  __shared__ float val[NA][16][16 * MB];
   __shared__ float rs[16 * MB];
 
-  const int tile = blockIdx.x;
+  const int tile0 = blockIdx.x * NTW;
+  const int n_tiles = (a.N + 15) / 16;
   const int m0 = blockIdx.y * 16 * MB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, grp = lane >> 4;
   const int Mloc = min(16 * MB, a.M - m0);
 
-  // ---- this lane's weight stream: packed 1 KB blocks, one per (tile, step, t)
-  const char *wbase = (const char *)a.wp + (size_t)tile * a.nsteps_w * NT * 1024 + lane * 16;
+  // ---- this lane's weight streams: packed 1 KB blocks, one per (tile, step, t)
+  const char *wbase[NTW];
+  bool wok[NTW];
+#pragma unroll
+  for (int tw = 0; tw < NTW; ++tw) {
+    wok[tw] = tile0 + tw < n_tiles;
+    wbase[tw] = (const char *)a.wp + (size_t)(wok[tw] ? tile0 + tw : 0) * a.nsteps_w * NT * 1024 + lane * 16;
+  }
   // ---- this lane's activation rows (one per M block)
   const T *xrow[MB];
   bool xok[MB];
@@ -117,32 +128,35 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
     xrow[mb] = (const T *)a.x + (size_t)(xok[mb] ? m : 0) * a.ldx;
   }
 
-  f32x4_t acc[NT][MB];
+  f32x4_t acc[NA][MB];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int t = 0; t < NA; ++t)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nsteps = a.nsteps_w;
-  F wa[U][NT], xa[U][MB], wb[U][NT], xb[U][MB];
+  F wa[U][NA], xa[U][MB], wb[U][NA], xb[U][MB];
 
-  auto load_chunk = [&](int s0, F (&w)[U][NT], F (&x)[U][MB]) {
+  auto load_chunk = [&](int s0, F (&w)[U][NA], F (&x)[U][MB]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = s0 + u * GEMM_WAVES;
       const int k = s * KSTEP + grp * EPB;
       const bool kin = (s < nsteps) && (k < a.K);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) w[u][t].v = load16(wbase + ((size_t)s * NT + t) * 1024, s < nsteps);
+      for (int tw = 0; tw < NTW; ++tw)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          w[u][tw * NT + t].v = load16(wbase[tw] + ((size_t)s * NT + t) * 1024, s < nsteps && wok[tw]);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) x[u][mb].v = load16_cached(xrow[mb] + k, kin && xok[mb]);
     }
   };
-  auto compute_chunk = [&](const F (&w)[U][NT], const F (&x)[U][MB]) {
+  auto compute_chunk = [&](const F (&w)[U][NA], const F (&x)[U][MB]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int t = 0; t < NA; ++t)
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[t][mb] = F::mma(w[u][t], x[u][mb], acc[t][mb]);
   };
@@ -164,7 +178,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
 
   // ---- split-K partials meet in LDS, summed in wave order
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int t = 0; t < NA; ++t)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -178,7 +192,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
     }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < NT * MB * 256; e += GEMM_THREADS) {
+  for (int e = threadIdx.x; e < NA * MB * 256; e += GEMM_THREADS) {
     const int t = e / (MB * 256), rem = e % (MB * 256);
     const int mb = rem / 256, li = rem % 256;
     const int ln = li >> 2, i = li & 3;
@@ -192,12 +206,16 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   }
   __syncthreads();
 
-  // ---- epilogues
+  // ---- epilogues, one weight tile at a time
+  for (int tw = 0; tw < NTW; ++tw) {
+  const int tile = tile0 + tw;
+  if (tile >= n_tiles) break;
+  float (*vt)[16][16 * MB] = &val[tw * NT];
   if constexpr (EPI == EPI_PLAIN) {
     for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
       const int ml = e / 16, nl = e % 16;
       const int n = tile * 16 + nl;
-      if (n < a.N) a.out[(size_t)(m0 + ml) * a.ld_out + n] = val[0][nl][ml];
+      if (n < a.N) a.out[(size_t)(m0 + ml) * a.ld_out + n] = vt[0][nl][ml];
     }
   } else if constexpr (EPI == EPI_QKV) {
     const int hd = a.head_dim;
@@ -208,7 +226,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int ml = e / 8, p = e % 8;           // pair p: dims 8j+p and hd/2+8j+p
       const int m = m0 + ml;
       const float r = (a.part != nullptr) ? rs[ml] : 1.f;
-      float x1 = val[0][p][ml] * r, x2 = val[0][p + 8][ml] * r;
+      float x1 = vt[0][p][ml] * r, x2 = vt[0][p + 8][ml] * r;
       const int i = 8 * j + p;
       const int c1 = col0 - (col0 % hd) + i;    // column of dim i in this head
       const int c2 = c1 + hd / 2;
@@ -239,7 +257,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int m = m0 + ml, n = tile * 16 + nl;
       const float *hin = a.h + (size_t)m * a.ld_h;
       float *hout = (a.row_bnd != nullptr) ? a.bnd_h + (size_t)a.row_bnd[m] * a.ld_h : a.h + (size_t)m * a.ld_h;
-      const float br = (a.bias != nullptr) ? a.alpha * (val[0][nl][ml] + a.bias[n]) : a.alpha * val[0][nl][ml];
+      const float br = (a.bias != nullptr) ? a.alpha * (vt[0][nl][ml] + a.bias[n]) : a.alpha * vt[0][nl][ml];
       const float hn = hin[n] + br;
       hout[n] = hn;
       if (a.xb != nullptr) ((T *)a.xb)[(size_t)m * a.ld_h + n] = to_t<T>(a.g_next[n] * hn);
@@ -261,7 +279,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int m = m0 + ml, n = tile * 16 + nl;
       if (n >= a.N) continue;
       const float r = (a.part != nullptr) ? rs[ml] : 1.f;
-      const float gt = val[0][nl][ml] * r, up = val[NT - 1][nl][ml] * r;
+      const float gt = vt[0][nl][ml] * r, up = vt[NT - 1][nl][ml] * r;
       const float sg = gt / (1.0f + expf(-gt));
       ((T *)a.act)[(size_t)m * a.ld_act + n] = to_t<T>(sg * up);
     }
@@ -271,7 +289,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int m = m0 + ml, n = tile * 16 + nl;
       if (n >= a.N) continue;
       const float r = (a.part != nullptr) ? rs[ml] : 1.f;
-      const float u = val[0][nl][ml] * r + a.bias[n];
+      const float u = vt[0][nl][ml] * r + a.bias[n];
       ((T *)a.act)[(size_t)m * a.ld_act + n] = to_t<T>(u / (1.0f + expf(-u)));
     }
   } else if constexpr (EPI == EPI_LOGITS) {
@@ -280,7 +298,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       const int ml = e / 16, nl = e % 16;
       const int m = m0 + ml, n = tile * 16 + nl;
       const float r = (a.part != nullptr) ? rs[ml] : 1.f;
-      float v = val[0][nl][ml] * r;
+      float v = vt[0][nl][ml] * r;
       if (n < a.N) {
         if (a.logits_tap != nullptr) a.logits_tap[(size_t)m * a.N + n] = v;
         // sampling mode (Algorithm 2): the Gumbel row of the row's slot
@@ -305,6 +323,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
       }
       a.amax[(size_t)(m0 + ml) * a.n_tiles + tile] = make_float2(best, __int_as_float(bi));
     }
+  }
+  __syncthreads();                             // epilogue scratch is reused by the next tile
   }
 }
 
@@ -362,13 +382,17 @@ static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
   if (a.M <= 16) {
     // deeper prefetch when a workgroup per CU streams a long tile, shallower
     // when many workgroups share each CU (measured on the 4096-wide layers)
-    if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8>), dim3(n_tiles, 1), block, 0, s, a);
-    else if (n_tiles <= 1024) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 4>), dim3(n_tiles, 1), block, 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2>), dim3(n_tiles, 1), block, 0, s, a);
-  } else if (a.M <= 32) {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4>), dim3(n_tiles, 1), block, 0, s, a);
+    if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    else if (n_tiles <= 1024) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    else hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2, 1>), dim3(n_tiles, 1), block, 0, s, a);
   } else {
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4>), dim3(n_tiles, (a.M + 63) / 64), block, 0, s, a);
+    // more rows: two weight tiles per workgroup share the activation loads
+    // (one tile for the gate/up pair at 64 rows, to bound the LDS)
+    constexpr int W4 = (EPI == EPI_SWIGLU) ? 1 : 2;
+    if (a.M <= 32)
+      hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
+    else
+      hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4, W4>), dim3((n_tiles + W4 - 1) / W4, (a.M + 63) / 64), block, 0, s, a);
   }
   return hipGetLastError();
 }
