@@ -574,8 +574,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     if (lane == 0) { prow[0] = 0; ppos[0] = c_pos; }
     tn = 0;
   } else {
-    const int gi = (item - n_chain_items) / a.jmax;
-    split = a.jmax - 1 - (item - n_chain_items) % a.jmax;
+    const int gi = (item - n_chain_items) / a.n_splits;
+    split = a.n_splits - 1 - (item - n_chain_items) % a.n_splits;
     r0 = a.grp_row0[gi];
     seq = a.grp_seq[gi];
     const int nr = a.grp_nrows[gi];
@@ -743,10 +743,11 @@ hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s) {
   if (n_groups <= 0 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
-  dim3 grid(n_groups, a.n_kv_heads, a.jmax);
+  if (a.n_splits < 1 || a.n_splits > a.jmax) return hipErrorInvalidValue;
+  dim3 grid(n_groups, a.n_kv_heads, a.n_splits);
   if (dtype == 1 && (a.head_dim == 128 || a.head_dim == 64)) {
     if (a.n_rows < 1 || a.row_seq == nullptr) return hipErrorInvalidValue;
-    const size_t items = 2 * (size_t)a.n_rows + (size_t)n_groups * a.jmax;
+    const size_t items = 2 * (size_t)a.n_rows + (size_t)n_groups * a.n_splits;
     if (items > 0x7fffffffull) return hipErrorInvalidValue;
     dim3 g2((unsigned)items, a.n_kv_heads);
     if (a.head_dim == 128) hipLaunchKernelGGL(attn_mfma_kernel<128>, g2, dim3(64), 0, s, a);

@@ -111,7 +111,8 @@ struct AttnArgs {
   const int *row_seq;         // sequence of each row (matrix-core kernel)
   int n_rows;                 // rows of the launch (matrix-core kernel)
   float *part;                // [R][H][jmax][hd + 2] split partials (o, max, sum)
-  int jmax;
+  int jmax;                   // split stride of `part`
+  int n_splits;               // splits the launch covers: max over its rows of pos / 64 + 1 (<= jmax)
   float scale;
 };
 
