@@ -183,17 +183,13 @@ struct ArgmaxArgs {
   int *u_out;                 // [M]
   int *cand;                  // [..][N] candidate table (nullable)
   const int *row_cand;        // [M] index into cand (slot*N + stage)
+  // verify/commit of the rows that complete an anchor's final stage
+  // (nullable): row_commit[m] = i >= 0 writes (token, k*) to commit_out[2i..]
+  const int *row_commit;
+  int N;
+  int *commit_out;
 };
 hipError_t launch_argmax(const ArgmaxArgs &a, hipStream_t s);
-
-struct CommitArgs {
-  int n;                      // sequences committing this round
-  const int *seq_cand;        // [n] candidate table offset of the anchor (slot*N)
-  int N;
-  const int *cand;
-  int *out;                   // [n][2] (token, kstar)
-};
-hipError_t launch_commit(const CommitArgs &a, hipStream_t s);
 
 struct CollapseArgs {
   int n_jobs;

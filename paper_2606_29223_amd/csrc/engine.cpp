@@ -115,7 +115,7 @@ struct dex_ctx {
   float *ex_h = nullptr, *ex_part = nullptr;
   void *ex_xb = nullptr;
   float2 *amax = nullptr;
-  int *u_dev = nullptr, *commit_dev = nullptr;
+  int *u_dev = nullptr;          // [R] decoded candidates, then [2 * commits] (token, k*)
   int *tab_dev = nullptr;
   size_t tab_cap = 0;
   int *job_dev = nullptr;
@@ -433,7 +433,7 @@ dex_status exit_adapter(dex_ctx *ctx, int k, int r0, int M) {
 // non-final depths for the adapters (nullptr: every row is final depth)
 dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h, const float *src_part,
                     const int *mask_n, const int *mask_tok, const int *cand_idx, int *cand, const int *row_seq,
-                    const int *row_pos, const int *stage_r0) {
+                    const int *row_pos, const int *stage_r0, const int *row_commit) {
   const hipStream_t st = ctx->stream;
   if (ctx->ad_m > 0 && stage_r0 != nullptr) {
     const int N = ctx->N;
@@ -465,6 +465,7 @@ dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h,
     ArgmaxArgs g{};
     g.amax = ctx->amax; g.n_tiles = n_tiles; g.M = M; g.u_out = ctx->u_dev;
     g.cand = cand; g.row_cand = cand_idx;
+    g.row_commit = row_commit; g.N = ctx->N; g.commit_out = ctx->u_dev + M;
     TimedLaunch tl(ctx, 7, 0.0);
     HIPCHK(launch_argmax(g, st));
   }
@@ -596,8 +597,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   A(&ctx->ex_xb, R * d * es);
   if (c->adapter_dim > 0) A(&ctx->ad_act, R * (size_t)c->adapter_dim * es);
   A((void **)&ctx->amax, R * ((ctx->V + 15) / 16) * sizeof(float2));
-  A((void **)&ctx->u_dev, R * 4 + 256);
-  A((void **)&ctx->commit_dev, (size_t)ctx->B * 2 * 4 + 256);
+  A((void **)&ctx->u_dev, (R + 2 * (size_t)ctx->B) * 4 + 256);
   A((void **)&ctx->job_dev, (size_t)(ctx->B * (ctx->S + 1)) * 6 * 4 + 256);
   ctx->tab_cap = (size_t)R * (16 + 2 * N + ctx->CH_MAX) + 4 * ctx->B + 1024;
   A((void **)&ctx->tab_dev, ctx->tab_cap * 4);
@@ -877,7 +877,8 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     }
   }
   // y_0: final-depth exit head at the last prompt position of every sequence
-  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr, d_exseq, d_expos, nullptr);
+  dex_status es2 = run_exit(ctx, B, d_exsrc, h, part, d_exzero, d_exzero, nullptr, nullptr, d_exseq, d_expos, nullptr,
+                            nullptr);
   if (es2 != DEX_OK) { cleanup(); return fail(ctx, es2); }
   HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, B * 4, hipMemcpyDeviceToHost, ctx->stream));
   HIPCHK(hipStreamSynchronize(ctx->stream));
@@ -955,7 +956,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   int *t_chain = t_mask + R * N;           // [R * CH_MAX]
   int *t_g0 = t_chain + R * ctx->CH_MAX;   // groups (stage-local row0), up to R
   int *t_gn = t_g0 + R, *t_gs = t_gn + R;
-  int *t_commit = t_gs + R;                // [B] anchor candidate offsets of committing sequences
+  int *t_rcommit = t_gs + R;               // [R] commit slot of a row completing its anchor, else -1
   std::vector<int> stage_r0(N + 1, 0), stage_g0(N + 1, 0);
   int chain_used = 0, ngroups = 0;
   const int G = ctx->H / ctx->Hkv;
@@ -1002,14 +1003,16 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   }
   stage_g0[N] = ngroups;
   std::vector<int> commit_seqs;
+  for (int r = 0; r < R; ++r) t_rcommit[r] = -1;
   for (int si = 0; si < B; ++si) {
     Seq &s = ctx->seqs[si];
     if (s.active && s.slots[0].c == N - 1) {
-      t_commit[commit_seqs.size()] = slot_global(ctx, si, s, 0) * N;
+      for (int r = 0; r < R; ++r)
+        if (rows[r].seq == si && rows[r].slot == 0) t_rcommit[r] = (int)commit_seqs.size();
       commit_seqs.push_back(si);
     }
   }
-  const size_t tab_ints = (size_t)(t_commit - T) + commit_seqs.size() + 1;
+  const size_t tab_ints = (size_t)(t_rcommit - T) + R;
   if (tab_ints > ctx->tab_cap) { ctx->err = "row table overflow"; return fail(ctx, DEX_E_CAPACITY); }
   HIPCHK(hipMemcpyAsync(ctx->tab_dev, T, tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
   const int *D = ctx->tab_dev;
@@ -1078,17 +1081,11 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   }
   // ---------------------------------------------------- exit + commit
   dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),
-                           dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos), stage_r0.data());
+                           dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos), stage_r0.data(), dptr(t_rcommit));
   if (xs != DEX_OK) return fail(ctx, xs);
-  {
-    CommitArgs c{};
-    c.n = (int)commit_seqs.size(); c.seq_cand = dptr(t_commit); c.N = N; c.cand = ctx->cand; c.out = ctx->commit_dev;
-    HIPCHK(launch_commit(c, ctx->stream));
-  }
-  HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, R * 4, hipMemcpyDeviceToHost, ctx->stream));
-  if (!commit_seqs.empty())
-    HIPCHK(hipMemcpyAsync(ctx->res_host + R, ctx->commit_dev, commit_seqs.size() * 2 * 4, hipMemcpyDeviceToHost,
-                          ctx->stream));
+  // candidates, then (token, k*) of the committing sequences, in one copy
+  HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, (R + 2 * commit_seqs.size()) * 4, hipMemcpyDeviceToHost,
+                        ctx->stream));
   HIPCHK(hipStreamSynchronize(ctx->stream));
   harvest_timing(ctx);
   ctx->rounds += 1;

@@ -1,9 +1,12 @@
 // Small kernels of the decode round: stage input (embedding gather or
-// boundary restore), argmax reduction, verify/commit, key/value collapse
-// gather, and a plain copy used to calibrate traffic counters.
+// boundary restore), argmax reduction with the verify/commit of completed
+// anchors, key/value collapse gather, and a plain copy used to calibrate
+// traffic counters.
 #include "dex_kernels.h"
 
 namespace dex {
+
+constexpr int PREP_THREADS = 64;              // 16-column groups per prep workgroup
 
 __device__ __forceinline__ float bf2f_m(bf16 b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ bf16 f2bf_m(float f) {
@@ -18,106 +21,138 @@ __device__ __forceinline__ bf16 f2bf_m(float f) {
 // continuing a slot restore the boundary state saved when the slot finished
 // its previous stage (partials copied unchanged, so a layer's norm sees the
 // same bits whether or not a stage boundary lies before it).
+//
+// Thread t of a row owns the 16-column group t: every load of the group is
+// requested before anything is stored, so a row costs one memory round trip.
 template <typename T>
-__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+__global__ __launch_bounds__(PREP_THREADS) void prep_kernel(PrepArgs a) {
+  constexpr int EPV = 16 / (int)sizeof(T);     // elements per 16-byte vector
   const int m = blockIdx.x;
+  const int t = blockIdx.y * PREP_THREADS + threadIdx.x;
+  if (t >= a.n_part) return;
   const int mo = (a.row_out != nullptr) ? a.row_out[m] : m;
-  float *h = a.h + (size_t)mo * a.d;
-  float *part = a.part + (size_t)mo * a.n_part;
-  T *xb = (T *)a.xb + (size_t)mo * a.d;
+  const int c0 = 16 * t;
+  float v[16], g[16];
+  float pin = 0.f;
   if (a.from_embed) {
-    const T *e = (const T *)a.embed + (size_t)a.row_tok[m] * a.d;
-    for (int i = threadIdx.x; i < a.d; i += blockDim.x) {
-      float v;
-      if constexpr (sizeof(T) == 2) v = bf2f_m(e[i]);
-      else v = e[i];
-      h[i] = v;
-      if (xb != nullptr) {
-        if constexpr (sizeof(T) == 2) xb[i] = f2bf_m(a.g[i] * v);
-        else xb[i] = a.g[i] * v;
+    const uint4 *e = (const uint4 *)((const T *)a.embed + (size_t)a.row_tok[m] * a.d + c0);
+    uint4 raw[16 / EPV];
+#pragma unroll
+    for (int q = 0; q < 16 / EPV; ++q) raw[q] = e[q];
+#pragma unroll
+    for (int q = 0; q < 16 / EPV; ++q) {
+      const uint32_t w[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) {
+        if constexpr (sizeof(T) == 2) v[q * EPV + k] = bf2f_m((bf16)((w[k >> 1] >> (16 * (k & 1))) & 0xffffu));
+        else v[q * EPV + k] = __uint_as_float(w[k]);
       }
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < a.n_part; t += blockDim.x) {
-      float s = 0.f;
-      for (int j = 0; j < 16; ++j) {
-        const float v = h[16 * t + j];
-        s += v * v;
-      }
-      part[t] = s;
     }
   } else {
-    const float *bh = a.bnd_h + (size_t)a.row_src[m] * a.d;
-    const float *bp = a.bnd_part + (size_t)a.row_src[m] * a.n_part;
-    for (int i = threadIdx.x; i < a.d; i += blockDim.x) {
-      const float v = bh[i];
-      h[i] = v;
-      if (xb != nullptr) {
-        if constexpr (sizeof(T) == 2) xb[i] = f2bf_m(a.g[i] * v);
-        else xb[i] = a.g[i] * v;
-      }
+    const float4 *bh = (const float4 *)(a.bnd_h + (size_t)a.row_src[m] * a.d + c0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 x = bh[q];
+      v[4 * q] = x.x; v[4 * q + 1] = x.y; v[4 * q + 2] = x.z; v[4 * q + 3] = x.w;
     }
-    for (int t = threadIdx.x; t < a.n_part; t += blockDim.x) part[t] = bp[t];
+    pin = a.bnd_part[(size_t)a.row_src[m] * a.n_part + t];
   }
+  const float4 *gp = (const float4 *)(a.g + c0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 x = gp[q];
+    g[4 * q] = x.x; g[4 * q + 1] = x.y; g[4 * q + 2] = x.z; g[4 * q + 3] = x.w;
+  }
+  float4 *h = (float4 *)(a.h + (size_t)mo * a.d + c0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) h[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  if (a.xb != nullptr) {
+    uint4 *xb = (uint4 *)((T *)a.xb + (size_t)mo * a.d + c0);
+#pragma unroll
+    for (int q = 0; q < 16 / EPV; ++q) {
+      uint32_t w[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (sizeof(T) == 2) {
+          const int e0 = q * EPV + 2 * k;
+          w[k] = (uint32_t)f2bf_m(g[e0] * v[e0]) | ((uint32_t)f2bf_m(g[e0 + 1] * v[e0 + 1]) << 16);
+        } else {
+          w[k] = __float_as_uint(g[q * EPV + k] * v[q * EPV + k]);
+        }
+      }
+      xb[q] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+  if (a.from_embed) {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) s += v[j] * v[j];
+    pin = s;
+  }
+  a.part[(size_t)mo * a.n_part + t] = pin;
 }
 
 hipError_t launch_prep(int dtype, const PrepArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (dtype == 1) hipLaunchKernelGGL(prep_kernel<bf16>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(prep_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+  if (a.d % 16 != 0 || a.n_part * 16 != a.d) return hipErrorInvalidValue;
+  const dim3 grid(a.M, (a.n_part + PREP_THREADS - 1) / PREP_THREADS);
+  if (dtype == 1) hipLaunchKernelGGL(prep_kernel<bf16>, grid, dim3(PREP_THREADS), 0, s, a);
+  else hipLaunchKernelGGL(prep_kernel<float>, grid, dim3(PREP_THREADS), 0, s, a);
   return hipGetLastError();
 }
 
 // argmax over the per-tile winners of each row; the lowest id wins ties.
-// Lane j scans a contiguous run of tiles in order, then a butterfly under the
-// total order (value, -id): the result is the sequential argmax.
-__global__ __launch_bounds__(64) void argmax_kernel(ArgmaxArgs a) {
-  const int m = blockIdx.x, lane = threadIdx.x;
+// The order (value, -id) is total, so any reduction order gives the
+// sequential argmax: thread j takes tiles j, j + 256, ... (all requested
+// before any is compared), then a wave butterfly and a pass over the waves.
+__device__ __forceinline__ void amax_take(float &bv, int &bi, float v, int i) {
+  if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
+}
+constexpr int AMAX_THREADS = 256;
+constexpr int AMAX_PER = 8;                    // tiles per thread per pass
+__global__ __launch_bounds__(AMAX_THREADS) void argmax_kernel(ArgmaxArgs a) {
+  __shared__ float sv[AMAX_THREADS / 64];
+  __shared__ int si[AMAX_THREADS / 64];
+  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float2 *src = a.amax + (size_t)m * a.n_tiles;
-  const int per = (a.n_tiles + 63) / 64;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int t = lane * per; t < min(a.n_tiles, (lane + 1) * per); ++t) {
-    const float v = src[t].x;
-    const int i = __float_as_int(src[t].y);
-    if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
+  for (int t0 = 0; t0 < a.n_tiles; t0 += AMAX_THREADS * AMAX_PER) {
+    float2 x[AMAX_PER];
+#pragma unroll
+    for (int k = 0; k < AMAX_PER; ++k) {
+      const int t = t0 + k * AMAX_THREADS + tid;
+      x[k] = t < a.n_tiles ? src[t] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+    }
+#pragma unroll
+    for (int k = 0; k < AMAX_PER; ++k) amax_take(bv, bi, x[k].x, __float_as_int(x[k].y));
   }
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float ov = __shfl_xor(bv, o, 64);
-    const int oi = __shfl_xor(bi, o, 64);
-    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-  }
-  if (lane == 0) {
+  for (int o = 32; o >= 1; o >>= 1) amax_take(bv, bi, __shfl_xor(bv, o, 64), __shfl_xor(bi, o, 64));
+  if (lane == 0) { sv[wave] = bv; si[wave] = bi; }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < AMAX_THREADS / 64; ++w) amax_take(bv, bi, sv[w], si[w]);
     a.u_out[m] = bi;
     if (a.cand != nullptr) a.cand[a.row_cand[m]] = bi;
+    // Validate and commit (Section 3.2, commit process) when this row is an
+    // anchor's final-depth node: its candidates u_0..u_{N-2} (earlier rounds)
+    // and u_{N-1} = bi; the committed token is u_{N-1}, the reusable branch
+    // the shallowest k <= N-2 with u_k == u_{N-1}, else N-1.
+    if (a.row_commit != nullptr && a.row_commit[m] >= 0) {
+      const int *u = a.cand + a.row_cand[m] - (a.N - 1);
+      int k = a.N - 1;
+      for (int j = 0; j < a.N - 1; ++j)
+        if (u[j] == bi) { k = j; break; }
+      a.commit_out[2 * a.row_commit[m]] = bi;
+      a.commit_out[2 * a.row_commit[m] + 1] = k;
+    }
   }
 }
 
 hipError_t launch_argmax(const ArgmaxArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_kernel, dim3(a.M), dim3(64), 0, s, a);
-  return hipGetLastError();
-}
-
-// Validate and commit (Section 3.2, commit process): the anchor's candidates
-// u_0..u_{N-1} by increasing depth; the committed token is u_{N-1}; the
-// reusable branch is the shallowest k <= N-2 with u_k == u_{N-1}, else N-1.
-__global__ void commit_kernel(CommitArgs a) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.n) return;
-  const int *u = a.cand + a.seq_cand[i];
-  const int y = u[a.N - 1];
-  int k = a.N - 1;
-  for (int j = 0; j < a.N - 1; ++j)
-    if (u[j] == y) { k = j; break; }
-  a.out[2 * i] = y;
-  a.out[2 * i + 1] = k;
-}
-
-hipError_t launch_commit(const CommitArgs &a, hipStream_t s) {
-  if (a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(commit_kernel, dim3((a.n + 63) / 64), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(argmax_kernel, dim3(a.M), dim3(AMAX_THREADS), 0, s, a);
   return hipGetLastError();
 }
 
