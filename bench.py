@@ -129,6 +129,7 @@ def main():
 
     m_hist = {}
     kstar_hist = {}
+    stages_hist = {}    # stages with rows per round (how much a round can overlap)
 
     ad_runs = [0]       # non-final stages with exit rows: each streams its adapter
 
@@ -140,6 +141,8 @@ def main():
             rounds += 1
             layers += dec.info.layers_streamed
             row_layers += dec.info.row_layers
+            ns = sum(1 for k in range(dec.N) if dec.info.rows_per_stage[k])
+            stages_hist[ns] = stages_hist.get(ns, 0) + 1
             for k in range(dec.N):
                 mk = dec.info.rows_per_stage[k]
                 if mk:
@@ -158,6 +161,7 @@ def main():
     warm_s = time.perf_counter() - tw
     m_hist.clear()
     kstar_hist.clear()
+    stages_hist.clear()
     ad_runs[0] = 0
     t0 = time.perf_counter()
     commits, rounds, layers, row_layers = steps(args.steps)
@@ -168,6 +172,8 @@ def main():
     # prefill plus every commit, over prefill and all decode rounds so far
     e2e = (B + warm_commits + commits) / (prefill_s + warm_s + elapsed)
     kstar_timed = dict(kstar_hist)
+    stages_timed = dict(stages_hist)
+    m_timed = dict(m_hist)
     ad_runs_timed = ad_runs[0]
 
     # instrumented run of the same length: per-kernel HIP event durations
@@ -262,7 +268,8 @@ def main():
                 "row_layers_per_commit": round(row_layers / max(commits, 1), 3),
                 "critical_path_layers_per_commit": round(L / N * rounds / max(commits, 1), 3),
                 "ar_layers_per_commit": L,
-                "rows_per_stage_hist": {str(k): v for k, v in sorted(m_hist.items())},
+                "rows_per_stage_hist": {str(k): v for k, v in sorted(m_timed.items())},
+                "stages_per_round_hist": {str(k): v for k, v in sorted(stages_timed.items())},
                 "matched_depth_hist": {str(k): v for k, v in sorted(kstar_timed.items())},
                 "weight_bytes_per_commit": bytes_per_commit,
                 "hbm_bytes_per_commit": hbm_bytes_per_commit,

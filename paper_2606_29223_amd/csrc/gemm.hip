@@ -304,13 +304,21 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
         // sampling mode (Algorithm 2): the Gumbel row of the row's slot
         if (a.temperature > 0.f)
           v = v / a.temperature + gumbel_noise(gumbel_key(a.sample_seed, a.row_seq[m], a.row_pos[m]), n);
-        const int nm = a.mask_n[m];
-        for (int q = 0; q < nm; ++q)
-          if (a.mask_tok[(size_t)m * a.mask_stride + q] == n) v = -INFINITY;
       } else {
         v = -INFINITY;
       }
       z[nl][ml] = v;
+    }
+    __syncthreads();
+    // DECS mask: each (row, masked token) pair clears its column if the token
+    // falls in this tile (one pass, every table load issued at once)
+    for (int e = threadIdx.x; e < Mloc * a.mask_stride; e += GEMM_THREADS) {
+      const int ml = e / a.mask_stride, q = e % a.mask_stride;
+      const int m = m0 + ml;
+      if (q < a.mask_n[m]) {
+        const int nn = a.mask_tok[(size_t)m * a.mask_stride + q] - tile * 16;
+        if (nn >= 0 && nn < 16) z[nn][ml] = -INFINITY;
+      }
     }
     __syncthreads();
     for (int ml = threadIdx.x; ml < Mloc; ml += GEMM_THREADS) {
