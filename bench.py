@@ -17,6 +17,10 @@ Prints one JSON line.  Besides the contract fields it carries
                attention's key/value reads) and the resulting HBM-roofline
                tokens/s of this schedule;
   e2e          committed tokens/s including the prefill (y_0 counts);
+  step_traffic HBM bytes per round counted by rocprofv3 (FETCH_SIZE +
+               WRITE_SIZE over the same rounds, profiles/step_traffic.json,
+               only while the kernel sources are unchanged) over this run's
+               time per round;
   cpu_baseline the oracle (float64 numpy) running the same decode on the host
                cores for a bounded sample.
 """
@@ -54,6 +58,7 @@ def parse():
     p.add_argument("--adapter-alpha", type=float, default=None,
                    help="attach synthetic inducing adapters with this gate to the non-final depths")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    p.add_argument("--step-traffic-json", default=os.path.join(ROOT, "profiles", "step_traffic.json"))
     return p.parse_args()
 
 
@@ -213,6 +218,21 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "bytes_per_launch": bytes_per, "avg_launch_us": round(avg_us, 2), "rows": m_mode}
 
+    # whole-round traffic counted for the same rounds with the current sources
+    step_traffic = None
+    if os.path.exists(args.step_traffic_json) and args.temperature == 0.0 and args.adapter_alpha is None:
+        from paper_2606_29223_amd.profile_summary import csrc_source_hash
+        try:
+            st = json.load(open(args.step_traffic_json))
+            if (st.get("source") == csrc_source_hash() and st.get("config") == cfg["name"]
+                    and st.get("warmup") == args.warmup and st.get("rounds") == args.steps):
+                gbs = st["counted_bytes_per_round"] / (elapsed / args.steps) / 1e9
+                step_traffic = {"counted_bytes_per_round": st["counted_bytes_per_round"],
+                                "algorithmic_bytes_per_round": st["algorithmic_bytes_per_round"],
+                                "achieved_GBps": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        except (OSError, ValueError, KeyError):
+            step_traffic = None
+
     ar_value = None
     if not args.no_ar:
         ar = dexlib.Decoder(cfg, dev_w, explored=[cfg["n_layers"]], width_cap=1, max_context=max_ctx, **samp)
@@ -262,6 +282,7 @@ def main():
                    "adapters": (f"synthetic, gate {args.adapter_alpha}" if args.adapter_alpha is not None
                                 else None)},
         "roofline": roofline,
+        "step_traffic": step_traffic,
         "cpu_baseline": cpu,
         "dex": {"commits": commits, "rounds": rounds, "rounds_per_commit": round(rounds / max(commits, 1), 4),
                 "weight_layers_streamed_per_commit": round(layers / max(commits, 1), 3),

@@ -4,6 +4,8 @@
       --command "..." --out profiles/NAME.txt
   python3 -m paper_2606_29223_amd.profile_summary traffic FETCH_DIR WRITE_DIR \
       --command "..." --out-json profiles/traffic.json --out profiles/NAME.txt
+  python3 -m paper_2606_29223_amd.profile_summary step FETCH_DIR WRITE_DIR \
+      --run-json RUN.json --bench-json BENCH.json --command "..." --out profiles/NAME.txt
   python3 -m paper_2606_29223_amd.profile_summary mfma PMC_DIR --command "..." \
       --out profiles/NAME.txt
 
@@ -12,7 +14,10 @@ attention kernels, the median duration of their decode launches.  `traffic`
 reads the FETCH_SIZE and WRITE_SIZE passes over `traffic_run`, derives the
 scale factor from the plain copy kernel (known bytes read and written) and
 reports bytes per launch for each decode GEMM class next to its algorithmic
-bytes.  The JSON records a hash of the GEMM kernel source so that a later
+bytes.  `step` adds up the counters over whole decode rounds of
+`traffic_run --decode-steps` and sets them against the rounds' algorithmic
+bytes and, with an unprofiled bench line, against the time per round.
+The traffic JSON records a hash of the GEMM kernel source so that a later
 change of the kernel invalidates the measurement.
 """
 
@@ -42,6 +47,16 @@ def gemm_source_hash() -> str:
     hdr = open(os.path.join(PKG, "csrc", "dex_kernels.h")).read()
     start = hdr.index("struct GemmArgs {")
     h.update(hdr[start:hdr.index("};", start)].encode())
+    return h.hexdigest()[:16]
+
+
+def csrc_source_hash() -> str:
+    """Hash of every kernel and engine source: whole-round traffic depends on
+    all of them."""
+    h = hashlib.sha1()
+    for f in sorted(glob.glob(os.path.join(PKG, "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -144,6 +159,48 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def step(args):
+    """HBM traffic of whole decode rounds: FETCH_SIZE and WRITE_SIZE of every
+    dispatch of traffic_run's measured rounds (the rounds are delimited by
+    the argmax launch that ends each exit head; the prompt's is the first),
+    scaled by the copy calibration, against the rounds' algorithmic bytes;
+    with the unprofiled bench's time per round, the counters' GB/s."""
+    run = json.load(open(args.run_json))
+    bench = json.load(open(args.bench_json)) if args.bench_json else None
+    tot = {}
+    for counter, d in (("FETCH_SIZE", args.fetch_dir), ("WRITE_SIZE", args.write_dir)):
+        disp = _per_dispatch(_counter_rows(d), counter)
+        copies = [v for n, v in disp if n.startswith("copy_kernel")]
+        scale = run["copy_bytes"] / (statistics.median(copies) * 1024.0)
+        ends = [i for i, (n, _) in enumerate(disp) if n.startswith("argmax_kernel")]
+        w, n = run["warmup"], run["rounds"]
+        lo, hi = ends[w] + 1, ends[w + n] + 1          # dispatches of the measured rounds
+        tot[counter] = sum(v for _, v in disp[lo:hi]) * 1024.0 * scale
+    per_round = (tot["FETCH_SIZE"] + tot["WRITE_SIZE"]) / run["rounds"]
+    alg = run["algorithmic_bytes_per_round"]
+    lines = [f"command: {args.command}", "",
+             f"workload {run['config']}: rounds {run['warmup'] + 1}..{run['warmup'] + run['rounds']} after the prompt, "
+             f"{run['commits']} commits, {run['weight_layers']} weight-layers streamed",
+             f"counted HBM bytes per round   {per_round / 1e9:8.3f} GB (fetch {tot['FETCH_SIZE'] / run['rounds'] / 1e9:.3f},"
+             f" write {tot['WRITE_SIZE'] / run['rounds'] / 1e9:.3f})",
+             f"algorithmic bytes per round   {alg / 1e9:8.3f} GB (weights of the stages run, exit head, K/V reads)",
+             f"counted / algorithmic         {per_round / alg:8.4f}"]
+    out = {"source": csrc_source_hash(), "command": args.command, "config": run["config"],
+           "warmup": run["warmup"], "rounds": run["rounds"], "counted_bytes_per_round": per_round,
+           "fetch_bytes_per_round": tot["FETCH_SIZE"] / run["rounds"],
+           "write_bytes_per_round": tot["WRITE_SIZE"] / run["rounds"], "algorithmic_bytes_per_round": alg}
+    if bench is not None and bench["config"]["workload"] == run["config"]:
+        ms = bench["ms_per_step"]
+        gbs = per_round / (ms * 1e-3) / 1e9
+        lines.append(f"unprofiled bench: {ms:.4f} ms per round -> {gbs:8.1f} GB/s counted = "
+                     f"{100 * gbs / 8000:.1f} % of 8 TB/s")
+        out.update({"ms_per_round": ms, "counted_GBps": gbs})
+    if args.out_json:
+        json.dump(out, open(args.out_json, "w"), indent=1)
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def mfma(args):
     """Matrix-core utilisation per kernel from one --pmc pass with
     SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 and
@@ -197,6 +254,14 @@ def main():
     t.add_argument("--command", required=True)
     t.add_argument("--out-json", required=True)
     t.add_argument("--out", required=True)
+    st = sub.add_parser("step")
+    st.add_argument("fetch_dir")
+    st.add_argument("write_dir")
+    st.add_argument("--run-json", required=True)
+    st.add_argument("--bench-json", default=None)
+    st.add_argument("--command", required=True)
+    st.add_argument("--out", required=True)
+    st.add_argument("--out-json", default=None)
     m = sub.add_parser("mfma")
     m.add_argument("pmc_dir")
     m.add_argument("--command", required=True)
@@ -205,7 +270,7 @@ def main():
     m.add_argument("--xcds", type=int, default=8)
     m.add_argument("--top", type=int, default=12)
     a = ap.parse_args()
-    {"stats": stats, "traffic": traffic, "mfma": mfma}[a.cmd](a)
+    {"stats": stats, "traffic": traffic, "step": step, "mfma": mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
