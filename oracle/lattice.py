@@ -28,7 +28,10 @@ One round:
     work): keep the anchor item and the W-1 others of lowest
     (hypothesis cost, path length, path) where a path is the list of fork
     stages leading from the anchor to the item and its hypothesis cost is
-    sum(f + 1) over it.
+    sum(f + 1) over it.  Parity unpinned: the paper fixes no pruning rule,
+    so a capped trace is pinned only by invariants (losslessness, at most W
+    rows a round, eligibility) and, for W >= 2^(N-1), by the paper's
+    uncapped lattice, which the rule must reproduce exactly.
   * DECS (greedy): a node's candidate is the argmax with the tokens already
     proposed by shallower nodes of the same slot masked out, except the
     anchor's final-depth node, which is never masked.  decs=False masks
