@@ -389,18 +389,36 @@ static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
   if (m_blocks <= 0) return hipErrorInvalidValue;
   if (a.M <= 16) {
     // deeper prefetch when a workgroup per CU streams a long tile, shallower
-    // when many workgroups share each CU (measured on the 4096-wide layers)
-    if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    // when many workgroups share each CU (measured on the 4096-wide layers);
+    // from 5 rows on, the wide matrices (gate/up, LM head) take two tiles per
+    // workgroup so that each activation load feeds two weight tiles
+    if (a.M > 4 && n_tiles > 512)
+      hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
+    else if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
     else if (n_tiles <= 1024) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
     else hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2, 1>), dim3(n_tiles, 1), block, 0, s, a);
   } else {
-    // more rows: two weight tiles per workgroup share the activation loads
-    // (one tile for the gate/up pair at 64 rows, to bound the LDS)
-    constexpr int W4 = (EPI == EPI_SWIGLU) ? 1 : 2;
-    if (a.M <= 32)
-      hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
-    else
-      hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4, W4>), dim3((n_tiles + W4 - 1) / W4, (a.M + 63) / 64), block, 0, s, a);
+    // more rows: the wide matrices take several weight tiles per workgroup
+    // so that each activation load feeds them all -- four for the 2000-tile
+    // LM head, two for gate/up; the 256/384-tile projections keep one tile
+    // per workgroup to fill the chip (measured per class at 24-64 rows); with
+    // 64-row blocks the reduction buffer takes most of the LDS
+    if (a.M <= 32) {
+      if constexpr (EPI == EPI_LOGITS)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 2, 4>), dim3((n_tiles + 3) / 4, 1), block, 0, s, a);
+      else if constexpr (EPI == EPI_SWIGLU)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    } else {
+      const unsigned mb = (unsigned)((a.M + 63) / 64);
+      if constexpr (EPI == EPI_LOGITS)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 2, 4>), dim3((n_tiles + 3) / 4, mb), block, 0, s, a);
+      else if constexpr (EPI == EPI_SWIGLU)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 2, 2>), dim3((n_tiles + 1) / 2, mb), block, 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4, 1>), dim3(n_tiles, mb), block, 0, s, a);
+    }
   }
   return hipGetLastError();
 }
