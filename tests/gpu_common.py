@@ -29,12 +29,14 @@ def host_weights(name: str, **over):
 
 @functools.lru_cache(maxsize=2)
 def device_weights(name: str):
+    torch_cuda()
     from paper_2606_29223_amd import dexlib
     cfg, w = host_weights(name)
     return dexlib.device_weights(cfg, w)
 
 
 def decoder(name: str, **kw):
+    torch_cuda()
     from paper_2606_29223_amd import dexlib
     cfg, _ = host_weights(name)
     return dexlib.Decoder(cfg, device_weights(name), **kw)

@@ -247,6 +247,27 @@ def test_small_bf16_lossless_and_oracle():
     assert worst <= LOGIT_RTOL, worst
 
 
+@pytest.mark.parametrize("X,W,decs", [([2, 4, 6, 8, 10, 12], 8, 1), ([6, 12], 2, 1), ([3, 6, 9, 12], 4, 0),
+                                      ([1, 12], 0, 1), ([4, 8, 12], 16, 1)])
+def test_small_bf16_explored_sets(X, W, decs):
+    """Other explored sets, width caps and vanilla mode on the 12-layer bf16
+    model (batch 2): DEX equals plain AR bit for bit and every round's plan,
+    commit and collapse equals the oracle lattice's on the GPU's candidates."""
+    torch_cuda()
+    cfg = configs.get(SMALL)
+    P, T = 64, 32
+    prompts = np.stack([gen.tokens(gen.mix64(s), P, cfg["vocab"]) for s in (7101, 7102)])
+    ar_dec = decoder(SMALL, explored=[cfg["n_layers"]], width_cap=1, batch=2, max_context=P + T)
+    ar_toks, _ = _run(ar_dec, prompts, T, collapse=False)
+    ar_dec.close()
+    dec = decoder(SMALL, explored=X, width_cap=W, decs=decs, batch=2, max_context=P + T)
+    toks, rounds = _run(dec, prompts, T)
+    dec.close()
+    assert np.array_equal(toks, ar_toks)
+    for b in range(2):
+        _replay(rounds, len(X), W, decs, P + T, toks[b][0], P, seq=b)
+
+
 @pytest.mark.parametrize("P", [1, 45, 97])
 def test_small_bf16_prefill_ragged_prompts(P):
     """Prompt lengths that are not a multiple of the 32-query / 64-key tiles
