@@ -231,6 +231,32 @@ class Decoder:
     def step(self) -> np.ndarray:
         return dex_step(self.ctx, self.batch, self.info)
 
+    def generate(self, prompts, n_tokens: int):
+        """Prefill, then dex_step until every sequence holds n_tokens
+        generated tokens (y_0 counts) or max_context stops it.  Returns
+        (tokens: list per sequence, stats: rounds, rows and layers streamed,
+        matched depth k* per commit)."""
+        first = self.prefill(prompts)
+        toks = [[int(first[b])] for b in range(self.batch)]
+        stats = {"rounds": 0, "rows": 0, "layers_streamed": 0, "row_layers": 0, "kstar": []}
+        while min(len(t) for t in toks) < n_tokens:
+            try:
+                c = self.step()
+            except DexError as e:
+                if e.status == DEX_E_CAPACITY:
+                    break
+                raise
+            inf = self.info
+            stats["rounds"] += 1
+            stats["rows"] += inf.n_rows
+            stats["layers_streamed"] += inf.layers_streamed
+            stats["row_layers"] += inf.row_layers
+            for b in range(self.batch):
+                if c[b] >= 0 and len(toks[b]) < n_tokens:
+                    toks[b].append(int(c[b]))
+                    stats["kstar"].append(int(inf.kstar[b]))
+        return toks, stats
+
     def set_logits_tap(self, tensor):
         st = self.lib.dex_debug_set_logits_tap(self.ctx, tensor.data_ptr() if tensor is not None else None,
                                                 tensor.shape[0] if tensor is not None else 0)

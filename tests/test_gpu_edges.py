@@ -10,7 +10,8 @@
   * the degenerate lattice of width 1: only the anchor advances, so every
     commit takes exactly N rounds from a fresh anchor, and the tokens are
     still AR's (Algorithm 1 with no parallel branch is sequential
-    early-exit verification at every depth).
+    early-exit verification at every depth);
+  * the binding's generate helper and the generation module.
 """
 import numpy as np
 import pytest
@@ -111,3 +112,27 @@ def test_width_one_commits_every_n_rounds():
     pl = [int(t) for t in prompt[0]]
     res = dex.dex_generate(m, pl, X, 1, True, T, keep_trace=False)
     assert res.tokens == toks[0] and res.rounds == rounds
+
+
+def test_generate_helper_and_cli(capsys, monkeypatch):
+    """Decoder.generate and the generation module: DEX tokens equal the
+    same library's AR tokens and the oracle's greedy AR, with one commit
+    per generated token after y_0."""
+    torch_cuda()
+    import json
+
+    from oracle import ar
+    from paper_2606_29223_amd import generate as gen_cli
+    cfg, w = host_weights(TINY)
+    T = 16
+    prompt = gen.prompts(cfg)
+    dec = decoder(TINY, max_context=cfg["prompt_len"] + T)
+    toks, st = dec.generate(prompt, T)
+    dec.close()
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    assert toks[0] == ar.ar_generate(m, [int(t) for t in prompt[0]], T)
+    assert len(st["kstar"]) == T - 1 and st["rounds"] >= T - 1
+    monkeypatch.setattr("sys.argv", ["generate", "--config", TINY, "--tokens", str(T), "--ar"])
+    gen_cli.main()
+    out = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
+    assert out["equals_ar"] and out["tokens"] == toks and out["commits"] == T - 1
