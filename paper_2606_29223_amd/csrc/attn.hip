@@ -226,72 +226,93 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 }
 
 // out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M}, M = max_j m_j,
-// over the splits j = 0 .. pos/64 of row r.  One wave per (row, head): lanes
-// over splits for the statistics (fixed butterflies), lanes over head
-// dimensions for the weighted sum, which runs over the splits in order.
+// over the splits j = 0 .. pos/64 of row r.  One workgroup of CMB_WAVES
+// waves per (row, head): wave s sums the splits j = s, s + CMB_WAVES, ... in
+// order (lanes over head dimensions) and the wave sums are added in wave
+// order; the statistics take one fixed reduction.  The arithmetic depends
+// only on the row's split count, never on the other rows of the launch.
+#ifndef CMB_WAVES
+#define CMB_WAVES 4
+#endif
 template <typename T, int HD>
-__global__ __launch_bounds__(64) void combine_kernel(CombineArgs a) {
+__global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) {
   constexpr int DPL = HD >= 64 ? HD / 64 : 1;
   constexpr int CH = 16;                       // splits per value chunk
+  constexpr int NT = 64 * CMB_WAVES;
   extern __shared__ float ws[];                // [jmax] split weights
-  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  __shared__ float red[CMB_WAVES][HD];         // per-wave weighted sums
+  __shared__ float sred[2][CMB_WAVES];         // per-wave max and denominator
+  const int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, s = tid >> 6;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
+  const int nmine = nsplit > s ? (nsplit - s + CMB_WAVES - 1) / CMB_WAVES : 0;
   const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (HD + 2);
   const int d0 = lane * DPL;
   const bool dok = d0 < HD;
   // the split values do not depend on the statistics: the first chunk is
   // requested before them, each next chunk before the current one is summed
   float va[CH][DPL], vb[CH][DPL];
-  auto load_chunk = [&](int j0, float (&v)[CH][DPL]) {
+  auto load_chunk = [&](int i0, float (&v)[CH][DPL]) {
 #pragma unroll
-    for (int jj = 0; jj < CH; ++jj)
+    for (int jj = 0; jj < CH; ++jj) {
+      const int j = s + (i0 + jj) * CMB_WAVES;
 #pragma unroll
       for (int q = 0; q < DPL; ++q)
-        v[jj][q] = (dok && j0 + jj < nsplit) ? src[(size_t)(j0 + jj) * (HD + 2) + d0 + q] : 0.f;
+        v[jj][q] = (dok && i0 + jj < nmine) ? src[(size_t)j * (HD + 2) + d0 + q] : 0.f;
+    }
   };
   load_chunk(0, va);
   float M = -INFINITY;
-  for (int j0 = 0; j0 < nsplit; j0 += 64) {
-    const int j = j0 + lane;
-    M = fmaxf(M, j < nsplit ? src[(size_t)j * (HD + 2) + HD] : -INFINITY);
-  }
+  for (int j = tid; j < nsplit; j += NT) M = fmaxf(M, src[(size_t)j * (HD + 2) + HD]);
   M = wave_max(M);
-  float lsum = 0.f;
-  for (int j0 = 0; j0 < nsplit; j0 += 64) {
-    const int j = j0 + lane;
-    float w = 0.f, lj = 0.f;
-    if (j < nsplit) {
-      w = expf(src[(size_t)j * (HD + 2) + HD] - M);
-      lj = src[(size_t)j * (HD + 2) + HD + 1];
-      ws[j] = w;
-    }
-    lsum += wave_sum(w * lj);
-  }
+  if (lane == 0) sred[0][s] = M;
   __syncthreads();
+  M = sred[0][0];
+#pragma unroll
+  for (int w = 1; w < CMB_WAVES; ++w) M = fmaxf(M, sred[0][w]);
+  float lp = 0.f;
+  for (int j = tid; j < nsplit; j += NT) {
+    const float w = expf(src[(size_t)j * (HD + 2) + HD] - M);
+    ws[j] = w;
+    lp = fmaf(w, src[(size_t)j * (HD + 2) + HD + 1], lp);
+  }
+  lp = wave_sum(lp);
+  if (lane == 0) sred[1][s] = lp;
+  __syncthreads();
+  float lsum = sred[1][0];
+#pragma unroll
+  for (int w = 1; w < CMB_WAVES; ++w) lsum += sred[1][w];
   float o[DPL];
 #pragma unroll
   for (int q = 0; q < DPL; ++q) o[q] = 0.f;
-  auto sum_chunk = [&](int j0, const float (&v)[CH][DPL]) {
+  auto sum_chunk = [&](int i0, const float (&v)[CH][DPL]) {
 #pragma unroll
     for (int jj = 0; jj < CH; ++jj) {
-      if (j0 + jj >= nsplit) break;
-      const float w = ws[j0 + jj];
+      if (i0 + jj >= nmine) break;
+      const float w = ws[s + (i0 + jj) * CMB_WAVES];
 #pragma unroll
       for (int q = 0; q < DPL; ++q) o[q] = fmaf(w, v[jj][q], o[q]);
     }
   };
-  for (int j0 = 0; j0 < nsplit; j0 += 2 * CH) {
-    if (j0 + CH < nsplit) load_chunk(j0 + CH, vb);
-    sum_chunk(j0, va);
-    if (j0 + CH >= nsplit) break;
-    if (j0 + 2 * CH < nsplit) load_chunk(j0 + 2 * CH, va);
-    sum_chunk(j0 + CH, vb);
+  for (int i0 = 0; i0 < nmine; i0 += 2 * CH) {
+    if (i0 + CH < nmine) load_chunk(i0 + CH, vb);
+    sum_chunk(i0, va);
+    if (i0 + CH >= nmine) break;
+    if (i0 + 2 * CH < nmine) load_chunk(i0 + 2 * CH, va);
+    sum_chunk(i0 + CH, vb);
   }
-  if (!dok) return;
+  if (dok) {
+#pragma unroll
+    for (int q = 0; q < DPL; ++q) red[s][d0 + q] = o[q];
+  }
+  __syncthreads();
+  if (s != 0 || !dok) return;
   T *out = (T *)a.out + (size_t)r * a.ld_out + h * HD + d0;
 #pragma unroll
   for (int q = 0; q < DPL; ++q) {
-    const float v = o[q] / lsum;
+    float v = red[0][d0 + q];
+#pragma unroll
+    for (int w = 1; w < CMB_WAVES; ++w) v += red[w][d0 + q];
+    v = v / lsum;
     if constexpr (sizeof(T) == 2) {
       uint32_t u = __float_as_uint(v);
       u += 0x7fffu + ((u >> 16) & 1u);
@@ -316,9 +337,9 @@ static hipError_t launch_attn_t(const AttnArgs &a, dim3 grid, hipStream_t s) {
 template <typename T>
 static hipError_t launch_comb_t(const CombineArgs &a, dim3 grid, hipStream_t s) {
   switch (a.head_dim) {
-    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64), a.jmax * 4, s, a); break;
-    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64), a.jmax * 4, s, a); break;
-    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64), a.jmax * 4, s, a); break;
+    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
+    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
+    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
