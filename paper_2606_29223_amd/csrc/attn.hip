@@ -374,6 +374,31 @@ __device__ __forceinline__ uint16_t pf_f2bf(float f) {
   u += 0x7fffu + ((u >> 16) & 1u);
   return (uint16_t)(u >> 16);
 }
+// Two floats rounded to bf16 (nearest even, as pf_f2bf) and packed, low first.
+typedef __attribute__((ext_vector_type(2))) __bf16 pf_bf16x2;
+typedef __attribute__((ext_vector_type(2))) float pf_f32x2;
+__device__ __forceinline__ uint32_t pf_pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((pf_f32x2{lo, hi}), pf_bf16x2));
+}
+// Max and sum over the 16 lanes of a row with DPP moves; the partner order
+// (lane ^ 1, lane ^ 2, then the other quad, then the other half-row) adds
+// exactly the operands of the xor butterfly, so every lane holds the same bits.
+template <int CTRL>
+__device__ __forceinline__ float pf_dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, pf_dpp<0xB1>(v));
+  v = fmaxf(v, pf_dpp<0x4E>(v));
+  v = fmaxf(v, pf_dpp<0x141>(v));
+  return fmaxf(v, pf_dpp<0x140>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += pf_dpp<0xB1>(v);
+  v += pf_dpp<0x4E>(v);
+  v += pf_dpp<0x141>(v);
+  return v + pf_dpp<0x140>(v);
+}
 
 template <int HD>
 __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
@@ -546,8 +571,15 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 // of 64 logical keys) -- with the two products on v_mfma_f32_16x16x32_bf16:
 //   S = Q K^T    the (row, query head) pairs as 16-row tiles, q rounded to
 //                bf16, against the split's four 16-key tiles;
-//   O = P V      P = exp(S - max) rounded to bf16 through an LDS tile, V
-//                transposed into LDS ([dim][key]).
+//   O = P V      P = exp(S - max) rounded to bf16 through a key-major LDS
+//                tile, V staged row-major in LDS; both operands come back
+//                in fragment order through the transpose read (tr_frag).
+// Keys are loaded in fragment order (16 keys x 64 bytes per instruction),
+// values as whole key rows (four per instruction): value loads of one key
+// row per lane touch 64 cache lines per instruction and held the split's
+// loads to 4.4 TB/s.  A split whose keys are consecutive committed entries
+// visible to every pair (the common case at long context) takes straight
+// address arithmetic and no mask.
 // Each output element of an MFMA depends only on its own pair's row and its
 // key (or dimension) column, and the softmax statistics reduce over the
 // split's keys in a fixed lane order, so a pair gets the same bits whichever
@@ -561,15 +593,32 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 //                positions, so two splits.  Dispatched first.
 //   group items  (row group, split without chain keys): every row of the
 //                group that reaches the split, committed keys only.
+// An MFMA 16x16x32 bf16 operand fragment from a key-major LDS tile with two
+// transpose reads (ds_read_b64_tr_b16).  Key rows of V are padded to
+// hd + 16 elements, so the four rows one quarter-wave reads start 8 banks
+// apart and the read is conflict-free.  Within each quarter-wave, lane j
+// receives element i from the address of lane 4 i + j / 4 at offset j % 4;
+// so if the lane (quarter q, 4 i + g) addresses row 8 q + i (then 8 q + 4 + i)
+// at column 4 g of a tile, lane (column c, quarter q) gets rows 8 q .. 8 q + 7
+// of column c -- the k-slots of an A row or a B column.
+typedef __attribute__((ext_vector_type(4))) short tr_i16x4;
+__device__ __forceinline__ pf_bf16x8 tr_frag(const uint16_t *lo, const uint16_t *hi) {
+  const tr_i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) tr_i16x4 *)lo);
+  const tr_i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) tr_i16x4 *)hi);
+  const uint2 ua = __builtin_bit_cast(uint2, a), ub = __builtin_bit_cast(uint2, b);
+  return __builtin_bit_cast(pf_bf16x8, make_uint4(ua.x, ua.y, ub.x, ub.y));
+}
+
 template <int HD>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = HD / 32;                 // k-steps of S over head dims
   constexpr int DT = HD / 16;                 // 16-dim tiles of O
   constexpr int NKT = ATT_SPLIT / 16;         // 16-key tiles per split
   constexpr int V4 = HD / 8;                  // 16-byte chunks per key row
-  constexpr int VROW = ATT_SPLIT + 8;         // padded V^T / P row (bf16)
-  __shared__ __attribute__((aligned(16))) uint16_t vt[HD][VROW];
-  __shared__ __attribute__((aligned(16))) uint16_t pt[16][VROW];
+  constexpr int VR = HD + 16;                 // padded key row of V in LDS (bf16)
+  constexpr int PR = 16 + 4;                  // padded key row of P in LDS (bf16)
+  __shared__ __attribute__((aligned(16))) uint16_t vr[ATT_SPLIT][VR];
+  __shared__ __attribute__((aligned(16))) uint16_t pk[ATT_SPLIT][PR];
   __shared__ int prow[ATT_MAX_PAIRS];         // rows (relative to r0) of the pass
   __shared__ int ppos[ATT_MAX_PAIRS];         // positions of those rows
 
@@ -581,6 +630,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   int r0, seq, split, n_pass;
   int c_nc = 0, c_pos = -1, c_coff = 0;       // chain item: its row
   int tn;                                     // group item: committed keys of the split
+  bool full = false;                          // every key of the split is seen by every pair
   const bool chain_item = item < n_chain_items;
   if (chain_item) {
     r0 = item >> 1;
@@ -621,6 +671,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
       ppos[k] = mypos;
     }
     tn = max(0, min(ATT_SPLIT, ncmax - s0));
+    int minpos = mypos >= s0 ? mypos : INT_MAX;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) minpos = min(minpos, __shfl_xor(minpos, o, 64));
+    full = tn == ATT_SPLIT && s1 <= minpos;
   }
   __syncthreads();
   const int s0 = split * ATT_SPLIT;
@@ -636,33 +690,42 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 
   // K as B fragments in registers: kf[nt][st] = key s0 + 16 nt + r16, dims
   // 32 st + 8 grp .. +8
-  uint4 kf[NKT][KS];
+  // V: whole key rows per load instruction (lane: row c * RPI + lane / V4,
+  // 16-byte chunk lane % V4), stored row-major; the P.V operands are read
+  // back with the LDS transpose read (see tr_frag)
+  constexpr int RPI = 64 / V4;                // key rows per load instruction
+  const int vrow = lane / V4, vch = lane % V4;
+  uint4 kf[NKT][KS], vv[V4];
+  if (full) {                                 // consecutive cache entries s0 ..
+    const uint16_t *kb = kbase + (size_t)s0 * HD, *vb = vbase + (size_t)s0 * HD;
 #pragma unroll
-  for (int nt = 0; nt < NKT; ++nt) {
-    const int e = entry(nt * 16 + r16);
+    for (int nt = 0; nt < NKT; ++nt)
 #pragma unroll
-    for (int st = 0; st < KS; ++st)
-      kf[nt][st] = e >= 0 ? *(const uint4 *)(kbase + (size_t)e * HD + st * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
-  }
-  // V: lane j loads key j's row and writes it as column j of V^T
-  {
-    const int e = entry(lane);
-    uint4 vv[V4];
+      for (int st = 0; st < KS; ++st)
+        kf[nt][st] = *(const uint4 *)(kb + (nt * 16 + r16) * HD + st * 32 + grp * 8);
 #pragma unroll
-    for (int c = 0; c < V4; ++c)
-      vv[c] = e >= 0 ? *(const uint4 *)(vbase + (size_t)e * HD + c * 8) : make_uint4(0, 0, 0, 0);
+    for (int c = 0; c < V4; ++c) vv[c] = *(const uint4 *)(vb + (c * RPI + vrow) * HD + vch * 8);
+  } else {
+#pragma unroll
+    for (int nt = 0; nt < NKT; ++nt) {
+      const int e = entry(nt * 16 + r16);
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+        kf[nt][st] = e >= 0 ? *(const uint4 *)(kbase + (size_t)e * HD + st * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+    }
 #pragma unroll
     for (int c = 0; c < V4; ++c) {
-      const uint32_t w[4] = {vv[c].x, vv[c].y, vv[c].z, vv[c].w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        vt[c * 8 + 2 * q][lane] = (uint16_t)(w[q] & 0xffffu);
-        vt[c * 8 + 2 * q + 1][lane] = (uint16_t)(w[q] >> 16);
-      }
+      const int e = entry(c * RPI + vrow);
+      vv[c] = e >= 0 ? *(const uint4 *)(vbase + (size_t)e * HD + vch * 8) : make_uint4(0, 0, 0, 0);
     }
   }
+#pragma unroll
+  for (int c = 0; c < V4; ++c) *(uint4 *)&vr[c * RPI + vrow][vch * 8] = vv[c];
   __syncthreads();
 
+  // this lane as a transpose-read source: quarter tq, key ti within it,
+  // four-element column group tg
+  const int tq = lane >> 4, ti = (lane & 15) >> 2, tg = lane & 3;
   const int P = n_pass * G;
   for (int mt = 0; mt * 16 < P; ++mt) {
     // A fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
@@ -678,11 +741,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         x0 = *(const float4 *)(qsrc + st * 32);
         x1 = *(const float4 *)(qsrc + st * 32 + 4);
       }
-      uint4 u;
-      u.x = pf_f2bf(x0.x) | ((uint32_t)pf_f2bf(x0.y) << 16);
-      u.y = pf_f2bf(x0.z) | ((uint32_t)pf_f2bf(x0.w) << 16);
-      u.z = pf_f2bf(x1.x) | ((uint32_t)pf_f2bf(x1.y) << 16);
-      u.w = pf_f2bf(x1.z) | ((uint32_t)pf_f2bf(x1.w) << 16);
+      const uint4 u = make_uint4(pf_pack_bf16(x0.x, x0.y), pf_pack_bf16(x0.z, x0.w),
+                                 pf_pack_bf16(x1.x, x1.y), pf_pack_bf16(x1.z, x1.w));
       qf[st] = __builtin_bit_cast(pf_bf16x8, u);
     }
     pf_f32x4 sc[NKT];
@@ -704,35 +764,41 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NKT; ++nt) {
         float v = sc[nt][i] * a.scale;
-        if (s0 + nt * 16 + r16 > pos) v = -INFINITY;
+        if (!full && s0 + nt * 16 + r16 > pos) v = -INFINITY;
         sc[nt][i] = v;
         mx = fmaxf(mx, v);
       }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      mx = row16_max(mx);
       float sum = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NKT; ++nt) {
         const float e = (mx == -INFINITY) ? 0.f : expf(sc[nt][i] - mx);
         sum += e;
-        pt[grp * 4 + i][nt * 16 + r16] = pf_f2bf(e);
+        sc[nt][i] = e;
       }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
+      sum = row16_sum(sum);
       mrow[i] = mx;
       lrow[i] = sum;
     }
+    // P (bf16) key-major: this lane's four pairs of key 16 nt + r16
+#pragma unroll
+    for (int nt = 0; nt < NKT; ++nt)
+      *(uint2 *)&pk[nt * 16 + r16][grp * 4] =
+          make_uint2(pf_pack_bf16(sc[nt][0], sc[nt][1]), pf_pack_bf16(sc[nt][2], sc[nt][3]));
     __syncthreads();
     pf_f32x4 o[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < ATT_SPLIT / 32; ++st) {
-      const pf_bf16x8 pfr = __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&pt[r16][st * 32 + grp * 8]);
+      // A = P (pairs x keys 32 st ..): lane (pair r16, group grp) gets keys 32 st + 8 grp .. +8
+      const pf_bf16x8 pfr = tr_frag(&pk[32 * st + 8 * tq + ti][4 * tg], &pk[32 * st + 8 * tq + 4 + ti][4 * tg]);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            pfr, __builtin_bit_cast(pf_bf16x8, *(const uint4 *)&vt[dt * 16 + r16][st * 32 + grp * 8]), o[dt], 0, 0, 0);
+            pfr,
+            tr_frag(&vr[32 * st + 8 * tq + ti][16 * dt + 4 * tg], &vr[32 * st + 8 * tq + 4 + ti][16 * dt + 4 * tg]),
+            o[dt], 0, 0, 0);
     }
     // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
 #pragma unroll
