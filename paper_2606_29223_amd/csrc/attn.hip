@@ -569,11 +569,14 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 //
 // Same partials as attn_kernel -- (o, max, sum) per (row, query head, split
 // of 64 logical keys) -- with the two products on v_mfma_f32_16x16x32_bf16:
-//   S = Q K^T    the (row, query head) pairs as 16-row tiles, q rounded to
-//                bf16, against the split's four 16-key tiles;
-//   O = P V      P = exp(S - max) rounded to bf16 through a key-major LDS
-//                tile, V staged row-major in LDS; both operands come back
-//                in fragment order through the transpose read (tr_frag).
+//   S^T = K Q^T  the split's four 16-key tiles against the (row, query
+//                head) pairs as 16 columns, q rounded to bf16: each lane
+//                then holds 16 keys of one pair;
+//   O = P V      P = exp(S - max) rounded to bf16 straight from those
+//                accumulators (the k-slots of the A operand are ordered as
+//                the keys the lane holds), V staged row-major in LDS and
+//                read back in the same key order through the transpose
+//                read (tr_frag).
 // Keys are loaded in fragment order (16 keys x 64 bytes per instruction),
 // values as whole key rows (four per instruction): value loads of one key
 // row per lane touch 64 cache lines per instruction and held the split's
@@ -582,8 +585,9 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 // address arithmetic and no mask.
 // Each output element of an MFMA depends only on its own pair's row and its
 // key (or dimension) column, and the softmax statistics reduce over the
-// split's keys in a fixed lane order, so a pair gets the same bits whichever
-// pairs share its tile.
+// split's keys in a fixed order (the lane's 16 keys in sequence, then the
+// four quarter-waves as an xor butterfly), so a pair gets the same bits
+// whichever pairs share its tile.
 //
 // Work items, one wave each, per kv head:
 //   chain items  (row, first or second split holding the row's lattice
@@ -594,13 +598,13 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 //   group items  (row group, split without chain keys): every row of the
 //                group that reaches the split, committed keys only.
 // An MFMA 16x16x32 bf16 operand fragment from a key-major LDS tile with two
-// transpose reads (ds_read_b64_tr_b16).  Key rows of V are padded to
-// hd + 16 elements, so the four rows one quarter-wave reads start 8 banks
-// apart and the read is conflict-free.  Within each quarter-wave, lane j
+// transpose reads (ds_read_b64_tr_b16).  Within each quarter-wave, lane j
 // receives element i from the address of lane 4 i + j / 4 at offset j % 4;
-// so if the lane (quarter q, 4 i + g) addresses row 8 q + i (then 8 q + 4 + i)
-// at column 4 g of a tile, lane (column c, quarter q) gets rows 8 q .. 8 q + 7
-// of column c -- the k-slots of an A row or a B column.
+// so if the lane (quarter q, 4 i + g) addresses row R(q, i) at column 4 g of
+// a tile, lane (column c, quarter q) gets rows R(q, 0..3) of column c as its
+// first four k-slots, and the second read's rows as the next four.  Key rows
+// of V are padded to hd + 16 elements, so four consecutive rows start 8 banks
+// apart and a quarter-wave's read is conflict-free.
 typedef __attribute__((ext_vector_type(4))) short tr_i16x4;
 __device__ __forceinline__ pf_bf16x8 tr_frag(const uint16_t *lo, const uint16_t *hi) {
   const tr_i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) tr_i16x4 *)lo);
@@ -616,9 +620,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   constexpr int NKT = ATT_SPLIT / 16;         // 16-key tiles per split
   constexpr int V4 = HD / 8;                  // 16-byte chunks per key row
   constexpr int VR = HD + 16;                 // padded key row of V in LDS (bf16)
-  constexpr int PR = 16 + 4;                  // padded key row of P in LDS (bf16)
   __shared__ __attribute__((aligned(16))) uint16_t vr[ATT_SPLIT][VR];
-  __shared__ __attribute__((aligned(16))) uint16_t pk[ATT_SPLIT][PR];
   __shared__ int prow[ATT_MAX_PAIRS];         // rows (relative to r0) of the pass
   __shared__ int ppos[ATT_MAX_PAIRS];         // positions of those rows
 
@@ -728,7 +730,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   const int tq = lane >> 4, ti = (lane & 15) >> 2, tg = lane & 3;
   const int P = n_pass * G;
   for (int mt = 0; mt * 16 < P; ++mt) {
-    // A fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
+    // Q^T fragments: pair mt*16 + r16, dims 32 st + 8 grp .. +8 (bf16)
     const int pa = mt * 16 + r16;
     const bool pok = pa < P;
     const int row = r0 + (pok ? prow[pa / G] : 0);
@@ -745,6 +747,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                                  pf_pack_bf16(x1.x, x1.y), pf_pack_bf16(x1.z, x1.w));
       qf[st] = __builtin_bit_cast(pf_bf16x8, u);
     }
+    // S^T = K Q^T: lane holds key 16 nt + 4 grp + i against its own pair pa
     pf_f32x4 sc[NKT];
 #pragma unroll
     for (int nt = 0; nt < NKT; ++nt) sc[nt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
@@ -752,53 +755,57 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     for (int st = 0; st < KS; ++st)
 #pragma unroll
       for (int nt = 0; nt < NKT; ++nt)
-        sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st], __builtin_bit_cast(pf_bf16x8, kf[nt][st]), sc[nt], 0, 0, 0);
-    // softmax over the split per pair: lane holds pairs mt*16 + 4 grp + i,
-    // keys 16 nt + r16
-    float mrow[4], lrow[4];
+        sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(pf_bf16x8, kf[nt][st]), qf[st], sc[nt], 0, 0, 0);
+    // softmax over the split for pair pa: 16 keys in this lane (nt, i order),
+    // then the lanes pa + 16, pa + 32 (xor butterfly over the four quarters)
+    const int pos = pok ? ppos[pa / G] : -1;
+    float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int pc = mt * 16 + grp * 4 + i;
-      const int pos = pc < P ? ppos[pc / G] : -1;
-      float mx = -INFINITY;
+    for (int nt = 0; nt < NKT; ++nt)
 #pragma unroll
-      for (int nt = 0; nt < NKT; ++nt) {
+      for (int i = 0; i < 4; ++i) {
         float v = sc[nt][i] * a.scale;
-        if (!full && s0 + nt * 16 + r16 > pos) v = -INFINITY;
+        if (!full && s0 + nt * 16 + grp * 4 + i > pos) v = -INFINITY;
         sc[nt][i] = v;
         mx = fmaxf(mx, v);
       }
-      mx = row16_max(mx);
-      float sum = 0.f;
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float sum = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NKT; ++nt) {
+    for (int nt = 0; nt < NKT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
         const float e = (mx == -INFINITY) ? 0.f : expf(sc[nt][i] - mx);
         sum += e;
         sc[nt][i] = e;
       }
-      sum = row16_sum(sum);
-      mrow[i] = mx;
-      lrow[i] = sum;
-    }
-    // P (bf16) key-major: this lane's four pairs of key 16 nt + r16
-#pragma unroll
-    for (int nt = 0; nt < NKT; ++nt)
-      *(uint2 *)&pk[nt * 16 + r16][grp * 4] =
-          make_uint2(pf_pack_bf16(sc[nt][0], sc[nt][1]), pf_pack_bf16(sc[nt][2], sc[nt][3]));
-    __syncthreads();
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
     pf_f32x4 o[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < ATT_SPLIT / 32; ++st) {
-      // A = P (pairs x keys 32 st ..): lane (pair r16, group grp) gets keys 32 st + 8 grp .. +8
-      const pf_bf16x8 pfr = tr_frag(&pk[32 * st + 8 * tq + ti][4 * tg], &pk[32 * st + 8 * tq + 4 + ti][4 * tg]);
+      // A = P (pairs x 32 keys): k-slot e of lane (pair r16, grp) is key
+      // 32 st + 4 grp + e (e < 4) or 32 st + 16 + 4 grp + e - 4, exactly the
+      // S^T values this lane holds; the V operand uses the same key order
+      const pf_bf16x8 pfr = __builtin_bit_cast(
+          pf_bf16x8, make_uint4(pf_pack_bf16(sc[2 * st][0], sc[2 * st][1]), pf_pack_bf16(sc[2 * st][2], sc[2 * st][3]),
+                                pf_pack_bf16(sc[2 * st + 1][0], sc[2 * st + 1][1]),
+                                pf_pack_bf16(sc[2 * st + 1][2], sc[2 * st + 1][3])));
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             pfr,
-            tr_frag(&vr[32 * st + 8 * tq + ti][16 * dt + 4 * tg], &vr[32 * st + 8 * tq + 4 + ti][16 * dt + 4 * tg]),
+            tr_frag(&vr[32 * st + 4 * tq + ti][16 * dt + 4 * tg], &vr[32 * st + 16 + 4 * tq + ti][16 * dt + 4 * tg]),
             o[dt], 0, 0, 0);
+    }
+    // statistics of pair pa from its first quarter
+    if (pok && grp == 0) {
+      float *dst = a.part + (((size_t)(r0 + prow[pa / G]) * a.n_heads + kvh * G + pa % G) * a.jmax + split) * (HD + 2);
+      dst[HD] = mx;
+      dst[HD + 1] = sum;
     }
     // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
 #pragma unroll
@@ -809,9 +816,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
       float *dst = a.part + (((size_t)prw * a.n_heads + kvh * G + pc % G) * a.jmax + split) * (HD + 2);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = o[dt][i];
-      if (r16 == 0) { dst[HD] = mrow[i]; dst[HD + 1] = lrow[i]; }
     }
-    __syncthreads();
   }
 }
 
