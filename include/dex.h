@@ -224,6 +224,34 @@ dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t r
 dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, const void *x, int32_t M,
                           float *y, void *hip_stream);
 
+/* Stand-alone decode attention (K4, the branch-masked attention of one
+ * layer) with its split combine, launched exactly as a step launches them
+ * for one stage.  Row r (sequence row_seq[r], absolute position row_pos[r],
+ * committed length row_nc[r]) attends with every query head h to the
+ * logical keys 0..row_pos[r] of kv head h / (n_heads / n_kv_heads): cache
+ * entries 0..row_nc[r]-1 of its sequence, then entry chain[chain_off[r] + t]
+ * for position row_nc[r] + t (its ancestor slots and its own slot), with
+ * scale 1/sqrt(head_dim) and softmax over those keys.  Consecutive rows of
+ * one sequence with equal row_nc form a row group as in a step.
+ *   dtype      dex_dtype of the caches and of out (bf16: matrix-core kernel
+ *              for head_dim 64 and 128)
+ *   head_dim   32, 64 or 128; n_heads a multiple of n_kv_heads, at most 8
+ *              query heads per kv head
+ *   k_cache, v_cache  device [batch][n_kv_heads][kv_entries][head_dim]
+ *   q          device float [n_rows][n_heads * head_dim] (RoPE applied)
+ *   out        device [n_rows][n_heads * head_dim] of dtype
+ *   row_*, chain_off, chain   host arrays (n_rows entries; chain_len)
+ * Requires 0 <= row_seq < batch, 0 <= row_nc <= row_pos + 1 <= kv_entries,
+ * at most 64 chain positions per row (row_pos - row_nc < 64), chain entries
+ * in [0, kv_entries) and chain_off[r] + row_pos[r] - row_nc[r] < chain_len;
+ * anything else returns DEX_E_INVAL before any launch.  Allocates and frees
+ * its own tables and split partials; synchronises hip_stream.            */
+dex_status dex_debug_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                               int32_t batch, int32_t kv_entries, const void *k_cache, const void *v_cache,
+                               const float *q, int32_t n_rows, const int32_t *row_seq, const int32_t *row_pos,
+                               const int32_t *row_nc, const int32_t *chain_off, const int32_t *chain,
+                               int32_t chain_len, void *out, void *hip_stream);
+
 /* The Gumbel source of sampling mode (Algorithm 2 draws one Gumbel row per
  * sampling slot; here the row of a slot is a function of (seed, sequence,
  * position of the slot's input token), so plain autoregressive sampling at

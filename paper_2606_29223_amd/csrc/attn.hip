@@ -595,8 +595,9 @@ __global__ __launch_bounds__(512) void prefill_attn_kernel(PrefillAttnArgs a) {
 //                from the committed cache below nc and from its chain
 //                entries from nc on.  A chain spans at most N + 1 <= 33
 //                positions, so two splits.  Dispatched first.
-//   group items  (row group, split without chain keys): every row of the
-//                group that reaches the split, committed keys only.
+//   group items  (row group, split): every row of the group that reaches
+//                the split and has no chain positions in it, committed
+//                keys only.
 // An MFMA 16x16x32 bf16 operand fragment from a key-major LDS tile with two
 // transpose reads (ds_read_b64_tr_b16).  Within each quarter-wave, lane j
 // receives element i from the address of lane 4 i + j / 4 at offset j % 4;
@@ -664,16 +665,20 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
       ncmax = max(ncmax, __shfl_xor(ncmax, o, 64));
     }
     if (s0 > maxpos) return;
-    if (__ballot(lr && max(mync, s0) <= min(mypos, s1)) != 0ull) return;   // a chain item's split
-    const unsigned long long reach = __ballot(mypos >= s0);
+    // a row whose chain positions fall in this split gets it from its chain
+    // item; the pass takes the group's other rows that reach the split
+    const bool chain_here = lr && max(mync, s0) <= min(mypos, s1);
+    const bool in_pass = mypos >= s0 && !chain_here;
+    const unsigned long long reach = __ballot(in_pass);
+    if (reach == 0ull) return;
     n_pass = __popcll(reach);
-    if (mypos >= s0) {
+    if (in_pass) {
       const int k = __popcll(reach & ((1ull << lane) - 1ull));
       prow[k] = lane;
       ppos[k] = mypos;
     }
     tn = max(0, min(ATT_SPLIT, ncmax - s0));
-    int minpos = mypos >= s0 ? mypos : INT_MAX;
+    int minpos = in_pass ? mypos : INT_MAX;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) minpos = min(minpos, __shfl_xor(minpos, o, 64));
     full = tn == ATT_SPLIT && s1 <= minpos;

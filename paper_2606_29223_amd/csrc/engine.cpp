@@ -1331,6 +1331,73 @@ dex_status dex_debug_gemm(int32_t dtype, const void *W, int32_t N, int32_t K, co
   return e == hipSuccess ? DEX_OK : DEX_E_HIP;
 }
 
+dex_status dex_debug_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                               int32_t batch, int32_t kv_entries, const void *k_cache, const void *v_cache,
+                               const float *q, int32_t n_rows, const int32_t *row_seq, const int32_t *row_pos,
+                               const int32_t *row_nc, const int32_t *chain_off, const int32_t *chain,
+                               int32_t chain_len, void *out, void *stream) {
+  if (dtype != DEX_F32 && dtype != DEX_BF16) return DEX_E_INVAL;
+  if (head_dim != 32 && head_dim != 64 && head_dim != 128) return DEX_E_INVAL;
+  if (n_kv_heads < 1 || n_heads < n_kv_heads || n_heads % n_kv_heads || n_heads / n_kv_heads > 8) return DEX_E_INVAL;
+  if (batch < 1 || kv_entries < 1 || n_rows < 1 || chain_len < 0) return DEX_E_INVAL;
+  if (!k_cache || !v_cache || !q || !out || !row_seq || !row_pos || !row_nc || !chain_off) return DEX_E_INVAL;
+  if (chain_len > 0 && !chain) return DEX_E_INVAL;
+  int maxpos = 0;
+  for (int r = 0; r < n_rows; ++r) {
+    const int sq = row_seq[r], pos = row_pos[r], nc = row_nc[r], co = chain_off[r];
+    if (sq < 0 || sq >= batch || pos < 0 || pos >= kv_entries || nc < 0 || nc > pos + 1) return DEX_E_INVAL;
+    if (pos - nc >= ATT_SPLIT) return DEX_E_INVAL;
+    if (nc <= pos && (co < 0 || (int64_t)co + (pos - nc) >= chain_len)) return DEX_E_INVAL;
+    for (int t = 0; nc + t <= pos; ++t)
+      if (chain[co + t] < 0 || chain[co + t] >= kv_entries) return DEX_E_INVAL;
+    maxpos = std::max(maxpos, pos);
+  }
+  const int n_splits = maxpos / ATT_SPLIT + 1;
+  if (n_splits > ATT_MAX_SPLITS) return DEX_E_INVAL;
+  // row groups: consecutive rows of one sequence sharing their committed
+  // prefix, at most 64 (row, query head) pairs' worth of rows each
+  const int G = n_heads / n_kv_heads, grp_rows = std::max(1, ATT_MAX_PAIRS / G);
+  std::vector<int> g0, gn, gs;
+  for (int r = 0; r < n_rows;) {
+    int e = r;
+    while (e < n_rows && row_seq[e] == row_seq[r] && row_nc[e] == row_nc[r] && e - r < grp_rows) ++e;
+    g0.push_back(r); gn.push_back(e - r); gs.push_back(row_seq[r]);
+    r = e;
+  }
+  const int ng = (int)g0.size();
+  std::vector<int> tab;
+  auto put = [&](const int32_t *p, int n) { const size_t o = tab.size(); tab.insert(tab.end(), p, p + n); return o; };
+  const size_t o_pos = put(row_pos, n_rows), o_nc = put(row_nc, n_rows), o_seq = put(row_seq, n_rows);
+  const size_t o_coff = put(chain_off, n_rows), o_g0 = put(g0.data(), ng), o_gn = put(gn.data(), ng);
+  const size_t o_gs = put(gs.data(), ng), o_chain = tab.size();
+  if (chain_len > 0) tab.insert(tab.end(), chain, chain + chain_len);
+  else tab.push_back(0);
+  const hipStream_t st = (hipStream_t)stream;
+  const size_t part_bytes = (size_t)n_rows * n_heads * n_splits * (head_dim + 2) * 4;
+  int *dtab = nullptr;
+  float *part = nullptr;
+  if (hipMalloc((void **)&dtab, tab.size() * 4) != hipSuccess) return DEX_E_NOMEM;
+  if (hipMalloc((void **)&part, part_bytes) != hipSuccess) { (void)hipFree(dtab); return DEX_E_NOMEM; }
+  hipError_t e = hipMemcpyAsync(dtab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice, st);
+  AttnArgs a{};
+  a.q = q; a.ldq = n_heads * head_dim; a.kc = k_cache; a.vc = v_cache; a.kv_entries = kv_entries;
+  a.n_kv_heads = n_kv_heads; a.n_heads = n_heads; a.head_dim = head_dim; a.batch = batch;
+  a.grp_row0 = dtab + o_g0; a.grp_nrows = dtab + o_gn; a.grp_seq = dtab + o_gs;
+  a.row_pos = dtab + o_pos; a.row_nc = dtab + o_nc; a.row_chain_off = dtab + o_coff; a.chain = dtab + o_chain;
+  a.row_seq = dtab + o_seq; a.n_rows = n_rows; a.part = part; a.jmax = n_splits; a.n_splits = n_splits;
+  a.scale = 1.0f / std::sqrt((float)head_dim);
+  if (e == hipSuccess) e = launch_attention(dtype, a, ng, st);
+  CombineArgs c{};
+  c.part = part; c.row_pos = dtab + o_pos; c.jmax = n_splits; c.n_heads = n_heads; c.head_dim = head_dim;
+  c.out = out; c.ld_out = n_heads * head_dim;
+  if (e == hipSuccess) e = launch_combine(dtype, c, n_rows, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  else (void)hipStreamSynchronize(st);
+  (void)hipFree(part);
+  (void)hipFree(dtab);
+  return e == hipSuccess ? DEX_OK : DEX_E_HIP;
+}
+
 dex_status dex_debug_gumbel(uint64_t seed, int32_t seq, int32_t pos, int32_t V, float *out, void *stream) {
   if (!out || V < 1 || seq < 0 || pos < 0) return DEX_E_INVAL;
   hipError_t e = launch_gumbel(seed, seq, pos, V, out, (hipStream_t)stream);

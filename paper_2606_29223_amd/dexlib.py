@@ -25,7 +25,8 @@ EXPORTED = (
     "dex_create", "dex_prefill", "dex_step", "dex_destroy", "dex_last_error",
     "dex_debug_set_logits_tap", "dex_debug_lattice", "dex_debug_last_collapse",
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
-    "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_gumbel", "dex_debug_copy",
+    "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_attention",
+    "dex_debug_gumbel", "dex_debug_copy",
 )
 
 
@@ -100,6 +101,8 @@ def load(path: str | None = None):
     lib.dex_debug_time_kernel.argtypes = [vp, i32, i32, i32, P(ctypes.c_double), P(ctypes.c_double)]
     lib.dex_debug_gemm.argtypes = [i32, vp, i32, i32, vp, i32, vp, vp]
     lib.dex_debug_copy.argtypes = [vp, vp, i64, vp]
+    lib.dex_debug_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, i32, P(i32), P(i32), P(i32),
+                                        P(i32), P(i32), i32, vp, vp]
     lib.dex_debug_gumbel.argtypes = [ctypes.c_uint64, i32, i32, i32, vp, vp]
     for name in EXPORTED:
         if name not in ("dex_destroy", "dex_last_error"):

@@ -95,3 +95,22 @@ def test_null_and_state_errors(lib):
     assert lib.dex_debug_copy(None, None, 16, None) == dexlib.DEX_E_INVAL
     assert lib.dex_debug_gemm(1, None, 16, 16, None, 1, None, None) == dexlib.DEX_E_INVAL
     assert lib.dex_debug_gumbel(1, 0, 0, 16, None, None) == dexlib.DEX_E_INVAL
+
+
+def test_debug_attention_rejects_bad_tables(lib):
+    """Every malformed table is refused on the host, before any device call
+    (the base arguments below are valid and are never passed unchanged)."""
+    fake = 0x1000
+
+    def call(dtype=1, hd=128, H=32, Hkv=8, B=1, E=100, seq=(0,), pos=(10,), nc=(10,), coff=(0,), chain=(50,),
+             q=fake):
+        arr = lambda v: (ctypes.c_int32 * len(v))(*v)
+        return lib.dex_debug_attention(dtype, hd, H, Hkv, B, E, fake, fake, q, len(seq), arr(seq), arr(pos),
+                                       arr(nc), arr(coff), arr(chain), len(chain), fake, None)
+
+    bad = [dict(seq=(1,)), dict(nc=(12,)), dict(pos=(90,)), dict(chain=(100,)), dict(chain=(-1,)),
+           dict(coff=(1,)), dict(hd=48), dict(H=72), dict(H=30), dict(pos=(100,), nc=(100,)), dict(q=None),
+           dict(dtype=2), dict(B=0), dict(nc=(-1,))]
+    for kw in bad:
+        assert call(**kw) == dexlib.DEX_E_INVAL, kw
+
