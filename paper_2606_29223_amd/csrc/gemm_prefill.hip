@@ -10,7 +10,10 @@
 // order: the packed weight layout stores one MFMA A fragment of a 16-row tile
 // per 1 KB block, and an input fragment is 16 rows x 64 contiguous bytes.
 // Neighbouring waves share operands through L1/L2.  The next k-step is loaded
-// while the current one is multiplied.
+// while the current one is multiplied.  From M = 2048 rows on, a second form
+// (gemm_big_kernel) stages the operands through LDS in 256 x 256 workgroup
+// tiles; it computes every output element from the same MFMA operands in the
+// same order, so the two forms give the same bits.
 //
 // The epilogues are those of the decode kernel (RMSNorm row scale, RoPE and
 // the key/value cache write; residual add with the next norm's input and its
@@ -37,6 +40,86 @@ __device__ __forceinline__ uint32_t tb_f2bf(float f) {
 }
 __device__ __forceinline__ uint2 tb_pack4(float a, float b, float c, float d) {
   return make_uint2(tb_f2bf(a) | (tb_f2bf(b) << 16), tb_f2bf(c) | (tb_f2bf(d) << 16));
+}
+
+// Epilogue of one 16 x 16 output tile held by a wave: lane (g, r) holds
+// output columns tile*16 + 4g .. +3 of input row m (ok: m < M).  Every lane
+// of the wave calls it (the QKV and RESID forms exchange values across
+// lanes).  acc[0] is the tile (SwiGLU: the gate tile, acc[1] the up tile),
+// rsc the row's RMSNorm scale.
+template <int EPI, int NT>
+__device__ __forceinline__ void tb_epilogue(const GemmArgs &a, int tile, int m, bool ok, const tb_f32x4 (&acc)[NT],
+                                            float rsc, int grp) {
+  if constexpr (EPI == EPI_PLAIN) {
+    if (ok) {
+      float *o = a.out + (size_t)m * a.ld_out + tile * 16 + grp * 4;
+      *(float4 *)o = make_float4(acc[0][0], acc[0][1], acc[0][2], acc[0][3]);
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    const int hd = a.head_dim;
+    const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
+    const int col0 = qkv_col(tile, 0, hd);
+    const int head_col = col0 - col0 % hd;   // first column of this head
+    const int j = tile % (hd / 16);
+    const bool lo = grp < 2;                 // rows 0..7: dims i; rows 8..15: dims i + hd/2
+    const int i0 = 8 * j + (grp & 1) * 4;    // RoPE pair index of this lane's first row
+    float y[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = acc[0][i] * rsc;
+      const float partner = __shfl_xor(v, 32, 64);
+      y[i] = v;
+      if (ok && head_col < nq + nk) {        // q or k: rotate the pair
+        const float2 cs = a.rope[(size_t)a.row_pos[m] * (hd / 2) + i0 + i];
+        y[i] = lo ? v * cs.x - partner * cs.y : v * cs.x + partner * cs.y;
+      }
+    }
+    if (ok) {
+      const int dim0 = (lo ? 0 : hd / 2) + i0;
+      if (head_col < nq) {
+        *(float4 *)(a.out + (size_t)m * a.ld_out + head_col + dim0) = make_float4(y[0], y[1], y[2], y[3]);
+      } else {
+        const bool isk = head_col < nq + nk;
+        const int g = (isk ? head_col - nq : head_col - nq - nk) / hd;
+        uint16_t *cache = (uint16_t *)(isk ? a.kc : a.vc);
+        const size_t base = (((size_t)a.row_seq[m] * a.n_kv_heads + g) * a.kv_entries + a.row_entry[m]) * hd;
+        *(uint2 *)(cache + base + dim0) = tb_pack4(y[0], y[1], y[2], y[3]);
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    const int n0 = tile * 16 + grp * 4;
+    float hn[4] = {0.f, 0.f, 0.f, 0.f};
+    if (ok) {
+      float *hp = a.h + (size_t)m * a.ld_h + n0;
+      const float4 hv = *(const float4 *)hp;
+      hn[0] = hv.x + a.alpha * acc[0][0];
+      hn[1] = hv.y + a.alpha * acc[0][1];
+      hn[2] = hv.z + a.alpha * acc[0][2];
+      hn[3] = hv.w + a.alpha * acc[0][3];
+      *(float4 *)hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
+      if (a.xb != nullptr) {
+        const float *gn = a.g_next + n0;
+        *(uint2 *)((uint16_t *)a.xb + (size_t)m * a.ld_h + n0) =
+            tb_pack4(gn[0] * hn[0], gn[1] * hn[1], gn[2] * hn[2], gn[3] * hn[3]);
+      }
+    }
+    // sum of squares over the tile's 16 columns: four per lane, then
+    // across the four lane groups that hold the same input row
+    float sq = hn[0] * hn[0] + hn[1] * hn[1] + hn[2] * hn[2] + hn[3] * hn[3];
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
+    if (ok && grp == 0) a.part_out[(size_t)m * a.n_part_out + tile] = sq;
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    if (ok) {
+      float o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float gt = acc[0][i] * rsc, up = acc[NT - 1][i] * rsc;
+        o[i] = gt / (1.0f + expf(-gt)) * up;
+      }
+      *(uint2 *)((uint16_t *)a.act + (size_t)m * a.ld_act + tile * 16 + grp * 4) = tb_pack4(o[0], o[1], o[2], o[3]);
+    }
+  }
 }
 
 template <int EPI>
@@ -128,81 +211,148 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
 #pragma unroll
   for (int t = 0; t < TN; ++t) {
     if (!tok[t]) continue;                    // uniform across the wave
-    const int tile = tile0 + t;
 #pragma unroll
     for (int f = 0; f < TB_MF; ++f) {
       const int m = m_base + f * 16 + r16;
-      const bool ok = m < a.M;
-      if constexpr (EPI == EPI_PLAIN) {
-        if (ok) {
-          float *o = a.out + (size_t)m * a.ld_out + tile * 16 + grp * 4;
-          *(float4 *)o = make_float4(acc[t][0][f][0], acc[t][0][f][1], acc[t][0][f][2], acc[t][0][f][3]);
-        }
-      } else if constexpr (EPI == EPI_QKV) {
-        const int hd = a.head_dim;
-        const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
-        const int col0 = qkv_col(tile, 0, hd);
-        const int head_col = col0 - col0 % hd;   // first column of this head
-        const int j = tile % (hd / 16);
-        const bool lo = grp < 2;                 // rows 0..7: dims i; rows 8..15: dims i + hd/2
-        const int i0 = 8 * j + (grp & 1) * 4;    // RoPE pair index of this lane's first row
-        float y[4];
+      tb_f32x4 at[NT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float v = acc[t][0][f][i] * rsc[f];
-          const float partner = __shfl_xor(v, 32, 64);
-          y[i] = v;
-          if (ok && head_col < nq + nk) {        // q or k: rotate the pair
-            const float2 cs = a.rope[(size_t)a.row_pos[m] * (hd / 2) + i0 + i];
-            y[i] = lo ? v * cs.x - partner * cs.y : v * cs.x + partner * cs.y;
-          }
-        }
-        if (ok) {
-          const int dim0 = (lo ? 0 : hd / 2) + i0;
-          if (head_col < nq) {
-            *(float4 *)(a.out + (size_t)m * a.ld_out + head_col + dim0) = make_float4(y[0], y[1], y[2], y[3]);
-          } else {
-            const bool isk = head_col < nq + nk;
-            const int g = (isk ? head_col - nq : head_col - nq - nk) / hd;
-            uint16_t *cache = (uint16_t *)(isk ? a.kc : a.vc);
-            const size_t base = (((size_t)a.row_seq[m] * a.n_kv_heads + g) * a.kv_entries + a.row_entry[m]) * hd;
-            *(uint2 *)(cache + base + dim0) = tb_pack4(y[0], y[1], y[2], y[3]);
-          }
-        }
-      } else if constexpr (EPI == EPI_RESID) {
-        const int n0 = tile * 16 + grp * 4;
-        float hn[4] = {0.f, 0.f, 0.f, 0.f};
-        if (ok) {
-          float *hp = a.h + (size_t)m * a.ld_h + n0;
-          const float4 hv = *(const float4 *)hp;
-          hn[0] = hv.x + a.alpha * acc[t][0][f][0];
-          hn[1] = hv.y + a.alpha * acc[t][0][f][1];
-          hn[2] = hv.z + a.alpha * acc[t][0][f][2];
-          hn[3] = hv.w + a.alpha * acc[t][0][f][3];
-          *(float4 *)hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
-          if (a.xb != nullptr) {
-            const float *gn = a.g_next + n0;
-            *(uint2 *)((uint16_t *)a.xb + (size_t)m * a.ld_h + n0) =
-                tb_pack4(gn[0] * hn[0], gn[1] * hn[1], gn[2] * hn[2], gn[3] * hn[3]);
-          }
-        }
-        // sum of squares over the tile's 16 columns: four per lane, then
-        // across the four lane groups that hold the same input row
-        float sq = hn[0] * hn[0] + hn[1] * hn[1] + hn[2] * hn[2] + hn[3] * hn[3];
-        sq += __shfl_xor(sq, 16, 64);
-        sq += __shfl_xor(sq, 32, 64);
-        if (ok && grp == 0) a.part_out[(size_t)m * a.n_part_out + tile] = sq;
-      } else if constexpr (EPI == EPI_SWIGLU) {
-        if (ok) {
-          float o[4];
+      for (int nt = 0; nt < NT; ++nt) at[nt] = acc[t][nt][f];
+      tb_epilogue<EPI, NT>(a, tile0 + t, m, m < a.M, at, rsc[f], grp);
+    }
+  }
+}
+
+// Large-M form (M >= BG_MIN_M): a workgroup of eight waves owns 256 weight
+// rows (16 packed blocks per k-step: 16 tiles, or 8 gate/up pairs) x 256
+// input rows and stages both operands through LDS in fragment order, two
+// k-steps (64 KB) per stage, double buffered, so each operand byte fetched
+// from L2 feeds 16 MFMA tiles instead of 2.  Wave (wn, wm) multiplies weight
+// blocks 8 wn .. 8 wn + 7 by input fragments 4 wm .. 4 wm + 3 (128 x 64
+// outputs) with the operand roles of gemm_tiled_kernel, accumulating the
+// k-steps in order, and hands each tile to the shared epilogue.  Workgroups
+// are numbered so that each XCD takes a contiguous run of tiles, grouped
+// eight input blocks deep, which keeps the operands the XCD's waves share in
+// its own L2.
+constexpr int BG_THREADS = 512;
+constexpr int BG_ROWS = 256;      // input rows per workgroup
+constexpr int BG_BLK = 16;        // weight blocks per k-step per workgroup
+constexpr int BG_KS = 2;          // k-steps per LDS stage
+constexpr int BG_GROUP = 8;       // input blocks per tile group
+constexpr int BG_MIN_M = 2048;
+
+template <int EPI>
+__global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_blk_n, int n_wg) {
+  constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;   // interleaved gate/up blocks
+  constexpr int TPW = BG_BLK / NT;                  // output tiles per workgroup
+  constexpr int WB = 8;                             // weight blocks per wave
+  constexpr int WF = 4;                             // input fragments per wave
+  constexpr int NCH = BG_KS * 2 * BG_BLK * 64 / BG_THREADS;   // staged 16-byte chunks per thread
+  __shared__ tb_u32x4 lds[2][BG_KS][2 * BG_BLK][64];          // [buffer][k-step][weight blocks | fragments][lane]
+
+  // workgroup -> tile: XCD x runs workgroup ids x, x + 8, ...; give it the
+  // contiguous tile range [start, start + count)
+  const int xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
+  const int base = n_wg / 8, rem = n_wg % 8;
+  const int t = xcd * base + min(xcd, rem) + jx;
+  const int n_blk_m = n_wg / n_blk_n;
+  const int per_group = BG_GROUP * n_blk_n;
+  const int g = t / per_group, first_m = g * BG_GROUP;
+  const int gsize = min(BG_GROUP, n_blk_m - first_m);
+  const int mb = first_m + (t % per_group) % gsize, nb = (t % per_group) / gsize;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int n_tiles = a.N / 16, nsteps = a.nsteps_w;
+  const int tile0 = nb * TPW, m0 = mb * BG_ROWS;
+
+  tb_f32x4 acc[WB][WF];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float gt = acc[t][0][f][i] * rsc[f], up = acc[t][NT - 1][f][i] * rsc[f];
-            o[i] = gt / (1.0f + expf(-gt)) * up;
-          }
-          *(uint2 *)((uint16_t *)a.act + (size_t)m * a.ld_act + tile * 16 + grp * 4) = tb_pack4(o[0], o[1], o[2], o[3]);
-        }
+  for (int jb = 0; jb < WB; ++jb)
+#pragma unroll
+    for (int f = 0; f < WF; ++f) acc[jb][f] = tb_f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // chunk c = tid + BG_THREADS * i: k-step c / (2 BG_BLK 64), block
+  // (c / 64) % (2 BG_BLK) (weights first, then input fragments), lane c % 64
+  tb_u32x4 stg[NCH];
+  auto gload = [&](int stage) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + BG_THREADS * i;
+      const int ks = c / (2 * BG_BLK * 64), b = (c / 64) % (2 * BG_BLK), l = c % 64;
+      const int step = stage * BG_KS + ks;
+      tb_u32x4 v = tb_u32x4{0u, 0u, 0u, 0u};
+      if (b < BG_BLK) {
+        const int tile = tile0 + b / NT, nt = b % NT;
+        if (tile < n_tiles && step < nsteps)
+          v = *(const tb_u32x4 *)((const char *)a.wp + (((size_t)tile * nsteps + step) * NT + nt) * 1024 + l * 16);
+      } else {
+        const int m = m0 + (b - BG_BLK) * 16 + (l & 15), k = step * 32 + (l >> 4) * 8;
+        if (m < a.M && k < a.K) v = *(const tb_u32x4 *)((const uint16_t *)a.x + (size_t)m * a.ldx + k);
       }
+      stg[i] = v;
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int c = tid + BG_THREADS * i;
+      lds[buf][c / (2 * BG_BLK * 64)][(c / 64) % (2 * BG_BLK)][c % 64] = stg[i];
+    }
+  };
+  const int nstages = (nsteps + BG_KS - 1) / BG_KS;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nstages) gload(st + 1);      // in flight while this stage is multiplied
+#pragma unroll
+    for (int ks = 0; ks < BG_KS; ++ks) {
+      tb_u32x4 w[WB], x[WF];
+#pragma unroll
+      for (int jb = 0; jb < WB; ++jb) w[jb] = lds[buf][ks][wn * WB + jb][lane];
+#pragma unroll
+      for (int f = 0; f < WF; ++f) x[f] = lds[buf][ks][BG_BLK + wm * WF + f][lane];
+#pragma unroll
+      for (int jb = 0; jb < WB; ++jb)
+#pragma unroll
+        for (int f = 0; f < WF; ++f)
+          acc[jb][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(tb_bf16x8, w[jb]),
+                                                               __builtin_bit_cast(tb_bf16x8, x[f]), acc[jb][f], 0, 0, 0);
+    }
+    if (st + 1 < nstages) lstore(buf ^ 1);    // that buffer's readers passed the last barrier
+    __syncthreads();
+  }
+
+  // RMSNorm scale of each input row of the wave (lane j sums the partials of
+  // row m0 + 64 wm + j in order), handed to the lanes holding that row
+  float rsc[WF];
+  if (a.part != nullptr) {
+    const int m = m0 + wm * 64 + lane;
+    float ss = 0.f;
+    if (m < a.M) {
+      const float *p = a.part + (size_t)m * a.n_part;
+      for (int q = 0; q < a.n_part; ++q) ss += p[q];
+    }
+    const float r = 1.0f / sqrtf(ss * a.inv_d + a.eps);
+#pragma unroll
+    for (int f = 0; f < WF; ++f) rsc[f] = __shfl(r, f * 16 + r16, 64);
+  } else {
+#pragma unroll
+    for (int f = 0; f < WF; ++f) rsc[f] = 1.f;
+  }
+#pragma unroll
+  for (int p = 0; p < WB / NT; ++p) {
+    const int tile = tile0 + wn * (WB / NT) + p;
+    if (tile >= n_tiles) continue;            // uniform across the wave
+#pragma unroll
+    for (int f = 0; f < WF; ++f) {
+      const int m = m0 + wm * 64 + f * 16 + r16;
+      tb_f32x4 at[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) at[nt] = acc[p * NT + nt][f];
+      tb_epilogue<EPI, NT>(a, tile, m, m < a.M, at, rsc[f], grp);
     }
   }
 }
@@ -224,6 +374,21 @@ bool gemm_tiled_supported(int epi, const GemmArgs &a) {
 hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s) {
   if (!gemm_tiled_supported(epi, a)) return hipErrorInvalidValue;
   const int n_tiles = a.N / 16;
+  if (a.M >= BG_MIN_M) {
+    const int tpw = BG_BLK / (epi == EPI_SWIGLU ? 2 : 1);
+    const int n_blk_n = (n_tiles + tpw - 1) / tpw, n_blk_m = (a.M + BG_ROWS - 1) / BG_ROWS;
+    const long long n_wg = (long long)n_blk_n * n_blk_m;
+    if (n_wg > 0x7fffffffLL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)n_wg), block(BG_THREADS);
+    switch (epi) {
+      case EPI_PLAIN: hipLaunchKernelGGL(gemm_big_kernel<EPI_PLAIN>, grid, block, 0, s, a, n_blk_n, (int)n_wg); break;
+      case EPI_QKV: hipLaunchKernelGGL(gemm_big_kernel<EPI_QKV>, grid, block, 0, s, a, n_blk_n, (int)n_wg); break;
+      case EPI_RESID: hipLaunchKernelGGL(gemm_big_kernel<EPI_RESID>, grid, block, 0, s, a, n_blk_n, (int)n_wg); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL(gemm_big_kernel<EPI_SWIGLU>, grid, block, 0, s, a, n_blk_n, (int)n_wg); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   const int tiles_per_wg = epi == EPI_SWIGLU ? 4 : 8;
   dim3 grid((n_tiles + tiles_per_wg - 1) / tiles_per_wg, (a.M + TB_ROWS - 1) / TB_ROWS);
   dim3 block(TB_THREADS);

@@ -306,6 +306,38 @@ def test_small_bf16_prefill_ragged_prompts(P):
         assert seen == T - 1
 
 
+def test_large_prompt_batch_prefill_matches_batch_one():
+    """Two 1100-token prompts make 2200 prompt rows, so the prompt GEMMs run
+    on the LDS-staged large-M kernel; one prompt alone runs the 128 x 128
+    kernel.  Both feed the MFMA tiles the same operands in the same k-step
+    order and share the epilogues (RoPE and cache write, residual and norm
+    partials, SwiGLU), so sequence 0's prompt keys/values, y_0 and the next
+    tokens are the same bits either way."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    P, T = 1100, 4
+    cfg2 = configs.get(SMALL, prompt_len=P, batch=2, prompt_seeds=[7101, 7102])
+    cfg1 = configs.get(SMALL, prompt_len=P, batch=1, prompt_seeds=[7101])
+    prompt = gen.prompts(cfg2)
+    assert np.array_equal(gen.prompts(cfg1)[0], prompt[0])
+    res = []
+    for cfg, pr in ((cfg2, prompt), (cfg1, prompt[:1])):
+        dec = dexlib.Decoder(cfg, device_weights(SMALL), max_context=P + T)
+        first = dec.prefill(pr)
+        k, v = _snapshot(dec, torch)
+        kv = (k[:, 0, :, :P, :].copy(), v[:, 0, :, :P, :].copy())
+        toks = [int(first[0])]
+        while len(toks) < T:
+            c = dec.step()
+            if c[0] >= 0:
+                toks.append(int(c[0]))
+        dec.close()
+        res.append((kv, toks))
+    (kv2, t2), (kv1, t1) = res
+    assert np.array_equal(kv2[0], kv1[0]) and np.array_equal(kv2[1], kv1[1])
+    assert t2 == t1
+
+
 def test_stage_streams_do_not_change_results():
     """Spreading a round's stages over several streams changes only the
     schedule: tokens, lattice traces and every row's exit logits are the same
