@@ -224,9 +224,12 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
 
 // Large-M form (M >= BG_MIN_M): a workgroup of eight waves owns 256 weight
 // rows (16 packed blocks per k-step: 16 tiles, or 8 gate/up pairs) x 256
-// input rows and stages both operands through LDS in fragment order, two
-// k-steps (64 KB) per stage, double buffered, so each operand byte fetched
-// from L2 feeds 16 MFMA tiles instead of 2.  Wave (wn, wm) multiplies weight
+// input rows and stages both operands through LDS in fragment order, so each
+// operand byte fetched from L2 feeds 16 MFMA tiles instead of 2.  The k-steps
+// (32 KB each) move global -> LDS with direct transfers (global_load_lds,
+// 16 bytes per lane at LDS base + 16 x lane) into a ring of four slots,
+// three steps ahead of the products: no staging registers, and each wave
+// waits (vmcnt) only for its own oldest step before the per-step barrier.  Wave (wn, wm) multiplies weight
 // blocks 8 wn .. 8 wn + 7 by input fragments 4 wm .. 4 wm + 3 (128 x 64
 // outputs) with the operand roles of gemm_tiled_kernel, accumulating the
 // k-steps in order, and hands each tile to the shared epilogue.  Workgroups
@@ -236,9 +239,13 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
 constexpr int BG_THREADS = 512;
 constexpr int BG_ROWS = 256;      // input rows per workgroup
 constexpr int BG_BLK = 16;        // weight blocks per k-step per workgroup
-constexpr int BG_KS = 2;          // k-steps per LDS stage
+constexpr int BG_NBUF = 4;        // LDS stages in the ring (three in flight)
 constexpr int BG_GROUP = 8;       // input blocks per tile group
 constexpr int BG_MIN_M = 2048;
+
+__device__ tb_u32x4 bg_zero[64];  // source of the zero lanes outside the operands
+
+#define BG_LDS(p) ((__attribute__((address_space(3))) void *)(p))
 
 template <int EPI>
 __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_blk_n, int n_wg) {
@@ -246,11 +253,9 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
   constexpr int TPW = BG_BLK / NT;                  // output tiles per workgroup
   constexpr int WB = 8;                             // weight blocks per wave
   constexpr int WF = 4;                             // input fragments per wave
-  constexpr int NCH = BG_KS * 2 * BG_BLK * 64 / BG_THREADS;   // staged 16-byte chunks per thread
-  __shared__ tb_u32x4 lds[2][BG_KS][2 * BG_BLK][64];          // [buffer][k-step][weight blocks | fragments][lane]
+  constexpr int NBLK = 2 * BG_BLK;                  // 1 KB blocks per stage
+  __shared__ tb_u32x4 lds[BG_NBUF][NBLK][64];       // [stage slot][weight blocks | fragments][lane]
 
-  // workgroup -> tile: XCD x runs workgroup ids x, x + 8, ...; give it the
-  // contiguous tile range [start, start + count)
   const int xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
   const int base = n_wg / 8, rem = n_wg % 8;
   const int t = xcd * base + min(xcd, rem) + jx;
@@ -272,57 +277,53 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
 #pragma unroll
     for (int f = 0; f < WF; ++f) acc[jb][f] = tb_f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // chunk c = tid + BG_THREADS * i: k-step c / (2 BG_BLK 64), block
-  // (c / 64) % (2 BG_BLK) (weights first, then input fragments), lane c % 64
-  tb_u32x4 stg[NCH];
-  auto gload = [&](int stage) {
+  // one k-step into slot `slot`: wave w moves blocks w, w + 8 (weights) and
+  // w + 16, w + 24 (input fragments), 1 KB each, global -> LDS
+  // one k-step into slot `slot`: wave w moves weight blocks w, w + 8 and
+  // input fragments w, w + 8 (1 KB each) global -> LDS, one instruction per
+  // block; lanes outside the operands read zeros.  The source is chosen by
+  // selects, so every wave issues exactly NBLK / 8 transfers per step.
+  const uintptr_t zero = (uintptr_t)(bg_zero + lane);
+  auto issue = [&](int step, int slot) {
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = tid + BG_THREADS * i;
-      const int ks = c / (2 * BG_BLK * 64), b = (c / 64) % (2 * BG_BLK), l = c % 64;
-      const int step = stage * BG_KS + ks;
-      tb_u32x4 v = tb_u32x4{0u, 0u, 0u, 0u};
-      if (b < BG_BLK) {
+    for (int i = 0; i < NBLK / 8; ++i) {
+      const int b = wave + 8 * i;
+      uintptr_t src;
+      if (i < 2) {                            // weight block b
         const int tile = tile0 + b / NT, nt = b % NT;
-        if (tile < n_tiles && step < nsteps)
-          v = *(const tb_u32x4 *)((const char *)a.wp + (((size_t)tile * nsteps + step) * NT + nt) * 1024 + l * 16);
-      } else {
-        const int m = m0 + (b - BG_BLK) * 16 + (l & 15), k = step * 32 + (l >> 4) * 8;
-        if (m < a.M && k < a.K) v = *(const tb_u32x4 *)((const uint16_t *)a.x + (size_t)m * a.ldx + k);
+        const uintptr_t wa = (uintptr_t)a.wp + (((size_t)tile * nsteps + step) * NT + nt) * 1024 + lane * 16;
+        src = tile < n_tiles ? wa : zero;
+      } else {                                // input fragment b - 16
+        const int m = m0 + (b - BG_BLK) * 16 + r16, k = step * 32 + grp * 8;
+        const uintptr_t xa = (uintptr_t)((const uint16_t *)a.x + (size_t)m * a.ldx + k);
+        src = ((m < a.M) & (k < a.K)) ? xa : zero;
       }
-      stg[i] = v;
+      __builtin_amdgcn_global_load_lds((const void *)src, BG_LDS(&lds[slot][b][0]), 16, 0, 0);
     }
   };
-  auto lstore = [&](int buf) {
+  for (int s = 0; s < BG_NBUF - 1 && s < nsteps; ++s) issue(s, s);
+  for (int st = 0; st < nsteps; ++st) {
+    // this wave's transfers of step st are done once at most those of the
+    // (up to two) younger steps are outstanding; the barrier makes every
+    // wave's done, and tells that all waves have finished step st - 1
+    const int younger = min(nsteps - 1 - st, BG_NBUF - 2);
+    if (younger >= 2) __builtin_amdgcn_s_waitcnt(0x0F70 | 8);
+    else if (younger == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | 4);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();
+    if (st + BG_NBUF - 1 < nsteps) issue(st + BG_NBUF - 1, (st + BG_NBUF - 1) % BG_NBUF);
+    const int slot = st % BG_NBUF;
+    tb_u32x4 w[WB], x[WF];
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = tid + BG_THREADS * i;
-      lds[buf][c / (2 * BG_BLK * 64)][(c / 64) % (2 * BG_BLK)][c % 64] = stg[i];
-    }
-  };
-  const int nstages = (nsteps + BG_KS - 1) / BG_KS;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int st = 0; st < nstages; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nstages) gload(st + 1);      // in flight while this stage is multiplied
+    for (int jb = 0; jb < WB; ++jb) w[jb] = lds[slot][wn * WB + jb][lane];
 #pragma unroll
-    for (int ks = 0; ks < BG_KS; ++ks) {
-      tb_u32x4 w[WB], x[WF];
+    for (int f = 0; f < WF; ++f) x[f] = lds[slot][BG_BLK + wm * WF + f][lane];
 #pragma unroll
-      for (int jb = 0; jb < WB; ++jb) w[jb] = lds[buf][ks][wn * WB + jb][lane];
+    for (int jb = 0; jb < WB; ++jb)
 #pragma unroll
-      for (int f = 0; f < WF; ++f) x[f] = lds[buf][ks][BG_BLK + wm * WF + f][lane];
-#pragma unroll
-      for (int jb = 0; jb < WB; ++jb)
-#pragma unroll
-        for (int f = 0; f < WF; ++f)
-          acc[jb][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(tb_bf16x8, w[jb]),
-                                                               __builtin_bit_cast(tb_bf16x8, x[f]), acc[jb][f], 0, 0, 0);
-    }
-    if (st + 1 < nstages) lstore(buf ^ 1);    // that buffer's readers passed the last barrier
-    __syncthreads();
+      for (int f = 0; f < WF; ++f)
+        acc[jb][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(tb_bf16x8, w[jb]),
+                                                             __builtin_bit_cast(tb_bf16x8, x[f]), acc[jb][f], 0, 0, 0);
   }
 
   // RMSNorm scale of each input row of the wave (lane j sums the partials of
