@@ -825,11 +825,205 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   }
 }
 
+// Causal prompt attention for head_dim 128 (bf16), G query heads per kv
+// head with G in {1, 2, 4, 8}.  Workgroup = (32 query rows, kv head,
+// sequence), wave w = query head kvh * G + w; blocks of 64 keys stream into
+// a two-slot LDS ring with direct global -> LDS transfers (one block ahead of
+// the products), shared by the G waves.  Per block each wave computes
+//   S^T = K Q^T   four 16-key tiles against its two 16-query tiles, so each
+//                 lane holds 16 keys of one query: the online-softmax
+//                 statistics are that lane's plus an xor butterfly over the
+//                 four quarter-waves, and the rescaling of O needs no
+//                 exchange;
+//   O^T += V^T P^T  V^T through the LDS transpose read, P^T straight from
+//                 the S^T accumulators (k-slot e of a lane is key
+//                 32 st + 4 grp + e or 32 st + 16 + 4 grp + e - 4, the keys it
+//                 holds), O^T rows = head dims, columns = queries.
+// K and V rows are 256 bytes with their 16-byte chunks XOR-swizzled (K: by
+// row mod 16, V: by 2 (row mod 8)) so that the 16 rows of a K fragment read
+// and the four rows of a transpose read land in distinct banks.  Query
+// blocks are dispatched longest first (the causal triangle).
+__device__ uint4 pa_zero[64];   // source of the key rows past the prompt
+
+template <int G>
+__global__ __launch_bounds__(64 * G) __attribute__((amdgpu_waves_per_eu(2))) void prefill_attn128_kernel(PrefillAttnArgs a) {
+  constexpr int HD = 128, KS = 4, DT = 8, NKT = 4, QB = 32, KB = 64;
+  constexpr int NTR = 2 * KB * HD * 2 / 1024;      // 1 KB transfers per key block (K then V)
+  constexpr int PER_WAVE = NTR / G;
+  __shared__ __attribute__((aligned(16))) uint4 kl[2][KB * 16];
+  __shared__ __attribute__((aligned(16))) uint4 vl[2][KB * 16];
+
+  const int P = a.prompt_len;
+  const int nqb = (P + QB - 1) / QB;
+  const int qb = nqb - 1 - (int)blockIdx.x;
+  const int kvh = blockIdx.y, seq = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int tq = lane >> 4, ti = (lane & 15) >> 2, tg = lane & 3;
+  const int h = kvh * G + wave;
+  const int q0 = qb * QB;
+  const size_t row_base = (size_t)seq * P;
+  const uint16_t *kbase = (const uint16_t *)a.kc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const uint16_t *vbase = (const uint16_t *)a.vc + ((size_t)seq * a.n_kv_heads + kvh) * a.kv_entries * HD;
+  const int nblk = (min(q0 + QB, P) - 1) / KB + 1;
+
+  // key block j into ring slot `slot`: transfer c (0..15 K, 16..31 V) moves
+  // rows 4 (c mod 16) .. +3; lane l fills chunk position l mod 16 of row
+  // 4 (c mod 16) + l / 16 with the swizzled global chunk
+  const uintptr_t zero = (uintptr_t)(pa_zero + lane);
+  auto issue = [&](int j, int slot) {
+#pragma unroll
+    for (int t = 0; t < PER_WAVE; ++t) {
+      const int c = wave + G * t;
+      const bool isv = c >= NTR / 2;
+      const int ci = c % (NTR / 2);
+      const int row = ci * 4 + (lane >> 4), pos = lane & 15;
+      const int chunk = isv ? (pos ^ (2 * (row & 7))) : (pos ^ (row & 15));
+      const int key = j * KB + row;
+      const uintptr_t g = (uintptr_t)((isv ? vbase : kbase) + (size_t)key * HD + chunk * 8);
+      const uintptr_t src = key < P ? g : zero;
+      uint4 *dst = isv ? &vl[slot][ci * 64] : &kl[slot][ci * 64];
+      __builtin_amdgcn_global_load_lds((const void *)src, (__attribute__((address_space(3))) void *)dst, 16, 0, 0);
+    }
+  };
+
+  // Q^T fragments (B operand): lane (query r16 of tile mt, grp) holds dims
+  // 32 st + 8 grp .. +8, rounded to bf16
+  pf_bf16x8 qf[2][KS];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int row = q0 + mt * 16 + r16;
+    const bool ok = row < P;
+    const float *src = a.q + (row_base + (ok ? row : 0)) * a.ldq + h * HD + grp * 8;
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+      if (ok) {
+        x0 = *(const float4 *)(src + st * 32);
+        x1 = *(const float4 *)(src + st * 32 + 4);
+      }
+      qf[mt][st] = __builtin_bit_cast(pf_bf16x8, make_uint4(pf_pack_bf16(x0.x, x0.y), pf_pack_bf16(x0.z, x0.w),
+                                                            pf_pack_bf16(x1.x, x1.y), pf_pack_bf16(x1.z, x1.w)));
+    }
+  }
+  pf_f32x4 o[2][DT];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[mt][dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun[2] = {-INFINITY, -INFINITY}, lrun[2] = {0.f, 0.f};
+  const float sl2 = a.scale * 1.44269504088896341f;   // scores in log2 units
+
+  issue(0, 0);
+  for (int j = 0; j < nblk; ++j) {
+    const int slot = j & 1, k0 = j * KB;
+    __builtin_amdgcn_s_waitcnt(0x0F70);      // this wave's transfers of block j are done
+    __builtin_amdgcn_s_barrier();            // every wave's, and every wave is past block j - 1
+    if (j + 1 < nblk) issue(j + 1, slot ^ 1);
+    const uint4 *K = kl[slot];
+    // S^T = K Q^T
+    pf_f32x4 sc[NKT][2];
+#pragma unroll
+    for (int nt = 0; nt < NKT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) sc[nt][mt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt) {
+        const pf_bf16x8 kfr = __builtin_bit_cast(pf_bf16x8, K[(nt * 16 + r16) * 16 + ((st * 4 + grp) ^ r16)]);
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          sc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kfr, qf[mt][st], sc[nt][mt], 0, 0, 0);
+      }
+    // online softmax of query q0 + 16 mt + r16 over keys k0 + 16 nt + 4 grp + i
+    const bool diag = k0 + KB - 1 > q0;
+    pf_bf16x8 pb[2][KB / 32];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const int query = q0 + mt * 16 + r16;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = sc[nt][mt][i] * sl2;
+          if (diag && k0 + nt * 16 + grp * 4 + i > query) v = -INFINITY;
+          sc[nt][mt][i] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(mrun[mt], mx);
+      const float mref = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = __builtin_amdgcn_exp2f(mrun[mt] - mref);
+      float sum = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NKT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = __builtin_amdgcn_exp2f(sc[nt][mt][i] - mref);
+          sc[nt][mt][i] = p;
+          sum += p;
+        }
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
+      lrun[mt] = lrun[mt] * alpha + sum;
+      mrun[mt] = mnew;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[mt][dt] *= alpha;
+#pragma unroll
+      for (int st = 0; st < KB / 32; ++st)
+        pb[mt][st] = __builtin_bit_cast(
+            pf_bf16x8, make_uint4(pf_pack_bf16(sc[2 * st][mt][0], sc[2 * st][mt][1]),
+                                  pf_pack_bf16(sc[2 * st][mt][2], sc[2 * st][mt][3]),
+                                  pf_pack_bf16(sc[2 * st + 1][mt][0], sc[2 * st + 1][mt][1]),
+                                  pf_pack_bf16(sc[2 * st + 1][mt][2], sc[2 * st + 1][mt][3])));
+    }
+    // O^T += V^T P^T
+    const uint16_t *V = (const uint16_t *)vl[slot];
+#pragma unroll
+    for (int st = 0; st < KB / 32; ++st) {
+      const int rlo = 32 * st + 4 * tq + ti, rhi = rlo + 16;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int c = 2 * dt + (tg >> 1);
+        const pf_bf16x8 vfr = tr_frag(V + (rlo * 16 + (c ^ (2 * (rlo & 7)))) * 8 + (tg & 1) * 4,
+                                      V + (rhi * 16 + (c ^ (2 * (rhi & 7)))) * 8 + (tg & 1) * 4);
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          o[mt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vfr, pb[mt][st], o[mt][dt], 0, 0, 0);
+      }
+    }
+  }
+  // O / l -> bf16: lane holds dims 16 dt + 4 grp .. +3 of query q0 + 16 mt + r16
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int query = q0 + mt * 16 + r16;
+    if (query >= P) continue;
+    const float inv = 1.f / lrun[mt];
+    uint16_t *dst = (uint16_t *)a.out + (row_base + query) * a.ld_out + h * HD + grp * 4;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *(uint2 *)(dst + dt * 16) = make_uint2(pf_pack_bf16(o[mt][dt][0] * inv, o[mt][dt][1] * inv),
+                                             pf_pack_bf16(o[mt][dt][2] * inv, o[mt][dt][3] * inv));
+  }
+}
+
 hipError_t launch_prefill_attention(const PrefillAttnArgs &a, hipStream_t s) {
   const int G = a.n_heads / a.n_kv_heads;
   if (G < 1 || G > 8 || a.prompt_len < 1) return hipErrorInvalidValue;
   dim3 grid((a.prompt_len + 31) / 32, a.n_kv_heads, a.batch);
   dim3 block(64 * G);
+  if (a.head_dim == 128 && (G == 1 || G == 2 || G == 4 || G == 8) && a.ld_out % 4 == 0) {
+    switch (G) {
+      case 1: hipLaunchKernelGGL(prefill_attn128_kernel<1>, grid, block, 0, s, a); break;
+      case 2: hipLaunchKernelGGL(prefill_attn128_kernel<2>, grid, block, 0, s, a); break;
+      case 4: hipLaunchKernelGGL(prefill_attn128_kernel<4>, grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL(prefill_attn128_kernel<8>, grid, block, 0, s, a); break;
+    }
+    return hipGetLastError();
+  }
   switch (a.head_dim) {
     case 64: hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, block, 0, s, a); break;
     case 128: hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, block, 0, s, a); break;

@@ -338,6 +338,48 @@ def test_large_prompt_batch_prefill_matches_batch_one():
     assert t2 == t1
 
 
+@pytest.mark.parametrize("P", [1, 45, 97, 300])
+def test_gqa128_prefill_ragged_prompts(P):
+    """The 32-layer model's attention shape (head_dim 128, four query heads
+    per kv head) on a 2-layer model small enough for the float64 oracle, with
+    prompt lengths that are not multiples of the 32-query / 64-key blocks of
+    the prompt attention (and the one-token prompt), at batch 2: y_0 and the
+    next tokens follow the oracle (near ties aside) and every decoded row's
+    exit logits agree within 2e-2 (max relative)."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = configs.scaled_down(configs.get("llama-32L-d4096-x8-w4"), n_layers=2, d_model=1024, d_ffn=2048,
+                              vocab=4096)
+    cfg.update(n_heads=8, n_kv_heads=2, head_dim=128, prompt_len=P, batch=2, prompt_seeds=[7201, 7202])
+    w = gen.generate_model(cfg)
+    T = 5
+    dec = dexlib.Decoder(cfg, dexlib.device_weights(cfg, w), explored=[cfg["n_layers"]], width_cap=1,
+                         max_context=P + T)
+    tap = torch.empty((8, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    prompt = gen.prompts(cfg)
+    toks, rounds = _run(dec, prompt, T, tap=tap, collapse=False)
+    dec.close()
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    for b in range(2):
+        pl = [int(t) for t in prompt[b]]
+        seq = [int(t) for t in toks[b]]
+        pf = m.prefill(pl)
+        z0 = m.exit_logits(pf[2])
+        if seq[0] != int(np.argmax(z0)):
+            srt = np.sort(z0)
+            assert srt[-1] - srt[-2] < GAP and z0.max() - z0[seq[0]] < GAP
+        z = ar.depth_logits(m, pl, seq, [cfg["n_layers"]], prefill=pf)
+        check_tokens_teacher_forced(z[:, -1], seq)
+        seen = 0
+        for rd in rounds:
+            for r, (s, slot, stage, pos, tok) in enumerate(rd["rows"]):
+                if s == b and pos - P < len(seq) - 1:
+                    assert max_rel_err(rd["logits"][r], z[pos - P, 0]) <= LOGIT_RTOL
+                    seen += 1
+        assert seen == T - 1
+
+
 def test_stage_streams_do_not_change_results():
     """Spreading a round's stages over several streams changes only the
     schedule: tokens, lattice traces and every row's exit logits are the same
