@@ -7,25 +7,26 @@
 // and its own slot, listed in `chain`.  Grouped-query heads: query head h
 // reads key/value head h / (H / Hkv).
 //
-// Work split: one wave per (row group, kv head, split of 64 logical keys).
-// A row group is consecutive rows of one sequence.  The split's committed
-// keys and values are loaded once with contiguous 1 KB loads and staged in
-// LDS (shared by every row and query head of the group); lane i scores the
-// key at position s0 + i from its LDS row, and a row whose logical key at
-// that position lives in a lattice slot reads it from its chain instead.  Per row: the G query heads' scores
-// run as independent FMA chains over the head dimensions, softmax statistics
-// are wave reductions, and lane i accumulates value dimensions
-// [i*hd/64, (i+1)*hd/64) over the split's keys in position order.  Each split
-// writes (o, max, sum) partials; a second kernel combines the splits.
+// Decode: the keys are cut into splits of 64 logical positions; a split
+// kernel writes one (o, max, sum) partial per (row, query head, split) and
+// combine_kernel merges a row's splits.  attn_mfma_kernel (bf16, head_dim 64
+// and 128) runs the two products on the matrix cores; attn_kernel (fp32
+// models, bf16 head_dim 32) is its VALU form: one workgroup per (row group,
+// kv head, split) stages the split's committed keys and values in LDS,
+// patches in each row's chain entries, and scores, normalises and sums per
+// row with one lane per key and then per value dimension.
 //
 // Every quantity a row computes depends only on its logical key sequence:
 // split and tile boundaries are fixed logical positions, each dot product
-// and each value sum runs in key/dimension order through one code path
-// whether the key is read from LDS or from a chain entry, and the combine
-// walks splits in order.  So a node evaluated speculatively (tail keys in
-// lattice slots) gets the bits plain decoding gets at the same position.
-// Splits of 64 keys keep a long context spread over many waves: 8192 keys x
-// 8 kv heads x 8 sequences is 9216 waves per layer.
+// and each value sum runs in a fixed key/dimension order whether the key is
+// read from the committed cache or a chain entry, and the combine's order
+// depends only on the row's split count.  So a node evaluated speculatively
+// (tail keys in lattice slots) gets the bits plain decoding gets at the same
+// position.  Splits of 64 keys keep a long context spread over many waves:
+// 8192 keys x 8 kv heads x 8 sequences is 9216 waves per layer.
+//
+// Prefill: prefill_attn128_kernel (head_dim 128) and prefill_attn_kernel
+// (head_dim 64) compute causal attention over the prompt's own keys.
 #include "dex_kernels.h"
 
 namespace dex {
