@@ -10,10 +10,10 @@
 // order: the packed weight layout stores one MFMA A fragment of a 16-row tile
 // per 1 KB block, and an input fragment is 16 rows x 64 contiguous bytes.
 // Neighbouring waves share operands through L1/L2.  The next k-step is loaded
-// while the current one is multiplied.  From M = 2048 rows on, a second form
-// (gemm_big_kernel) stages the operands through LDS in 256 x 256 workgroup
-// tiles; it computes every output element from the same MFMA operands in the
-// same order, so the two forms give the same bits.
+// while the current one is multiplied.  When its grid reaches 96 workgroups,
+// a second form (gemm_big_kernel) stages the operands through LDS in
+// 256 x 256 workgroup tiles; it computes every output element from the same
+// MFMA operands in the same order, so the two forms give the same bits.
 //
 // The epilogues are those of the decode kernel (RMSNorm row scale, RoPE and
 // the key/value cache write; residual add with the next norm's input and its
@@ -222,7 +222,8 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
   }
 }
 
-// Large-M form (M >= BG_MIN_M): a workgroup of eight waves owns 256 weight
+// Large form (whenever its grid has at least BG_MIN_WG workgroups; below
+// that the 128 x 128 form keeps more CUs busy): a workgroup of eight waves owns 256 weight
 // rows (16 packed blocks per k-step: 16 tiles, or 8 gate/up pairs) x 256
 // input rows and stages both operands through LDS in fragment order, so each
 // operand byte fetched from L2 feeds 16 MFMA tiles instead of 2.  The k-steps
@@ -241,7 +242,7 @@ constexpr int BG_ROWS = 256;      // input rows per workgroup
 constexpr int BG_BLK = 16;        // weight blocks per k-step per workgroup
 constexpr int BG_NBUF = 4;        // LDS stages in the ring (three in flight)
 constexpr int BG_GROUP = 8;       // input blocks per tile group
-constexpr int BG_MIN_M = 2048;
+constexpr int BG_MIN_WG = 96;    // smallest grid that takes this form
 
 __device__ tb_u32x4 bg_zero[64];  // source of the zero lanes outside the operands
 
@@ -375,10 +376,10 @@ bool gemm_tiled_supported(int epi, const GemmArgs &a) {
 hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s) {
   if (!gemm_tiled_supported(epi, a)) return hipErrorInvalidValue;
   const int n_tiles = a.N / 16;
-  if (a.M >= BG_MIN_M) {
-    const int tpw = BG_BLK / (epi == EPI_SWIGLU ? 2 : 1);
-    const int n_blk_n = (n_tiles + tpw - 1) / tpw, n_blk_m = (a.M + BG_ROWS - 1) / BG_ROWS;
-    const long long n_wg = (long long)n_blk_n * n_blk_m;
+  const int tpw = BG_BLK / (epi == EPI_SWIGLU ? 2 : 1);
+  const int n_blk_n = (n_tiles + tpw - 1) / tpw, n_blk_m = (a.M + BG_ROWS - 1) / BG_ROWS;
+  const long long n_wg = (long long)n_blk_n * n_blk_m;
+  if (n_wg >= BG_MIN_WG) {
     if (n_wg > 0x7fffffffLL) return hipErrorInvalidValue;
     dim3 grid((unsigned)n_wg), block(BG_THREADS);
     switch (epi) {

@@ -307,12 +307,13 @@ def test_small_bf16_prefill_ragged_prompts(P):
 
 
 def test_large_prompt_batch_prefill_matches_batch_one():
-    """Two 1100-token prompts make 2200 prompt rows, so the prompt GEMMs run
-    on the LDS-staged large-M kernel; one prompt alone runs the 128 x 128
-    kernel.  Both feed the MFMA tiles the same operands in the same k-step
-    order and share the epilogues (RoPE and cache write, residual and norm
-    partials, SwiGLU), so sequence 0's prompt keys/values, y_0 and the next
-    tokens are the same bits either way."""
+    """Two 1100-token prompts make 2200 prompt rows, so the gate/up prompt
+    GEMM gets 144 256 x 256 workgroups and runs on the LDS-staged kernel;
+    one prompt alone (80 such workgroups) runs the 128 x 128 kernel.  Both
+    feed the MFMA tiles the same operands in the same k-step order and share
+    the epilogues (RoPE and cache write, residual and norm partials, SwiGLU),
+    so sequence 0's prompt keys/values, y_0 and the next tokens are the same
+    bits either way."""
     torch = torch_cuda()
     from paper_2606_29223_amd import dexlib
     P, T = 1100, 4

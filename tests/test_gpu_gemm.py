@@ -69,21 +69,22 @@ def test_tiled_prefill_gemm_matches_float64(N, K, M):
     assert np.array_equal(y.view(np.uint32), _gemm(torch, 1, Wt, xt, M).view(np.uint32))
 
 
-@pytest.mark.parametrize("N,K", [(6144, 4096), (784, 768), (2048, 14336)])
-def test_large_prefill_gemm_matches_the_small_tiles(N, K):
-    """M >= 2048 takes the LDS-staged 256 x 256 kernel.  It feeds every MFMA
-    tile the same operands in the same k-step order as the 128 x 128 kernel,
-    so each row's bits equal those of a smaller launch of the same rows; and
-    float64 parity on rows at the workgroup edges and a ragged last block."""
+@pytest.mark.parametrize("N,K,M", [(6144, 4096, 2100), (2064, 14336, 3000), (1552, 768, 4000)])
+def test_large_prefill_gemm_matches_the_small_tiles(N, K, M):
+    """A grid of 96 or more 256 x 256 workgroups (here 216, 108 and 112, with
+    ragged last blocks in M and N) takes the LDS-staged kernel.  It feeds
+    every MFMA tile the same operands in the same k-step order as the
+    128 x 128 kernel, which 500-row launches of the same rows take (at most
+    48 such workgroups), so each row's bits are equal; and float64 parity
+    on rows at the workgroup edges and in the ragged last block."""
     torch = torch_cuda()
-    M = 2100
     Wt, xt, W64, x64 = _inputs(torch, 1, N, K, M, 500 + N)
     big = _gemm(torch, 1, Wt, xt, M)
-    rows = [0, 1, 255, 256, 1023, 2047, 2048, 2099] + list(np.random.default_rng(N).integers(0, M, 8))
+    rows = [0, 1, 255, 256, 1023, M - 257, M - 256, M - 1] + list(np.random.default_rng(N).integers(0, M, 8))
     ref = x64[rows] @ W64.T
     err = np.abs(big[rows] - ref).max()
     assert err <= 2e-5 * np.sqrt(K) * 0.05 + 1e-6, err
-    for lo, hi in ((0, 1000), (1100, 2100)):
+    for lo, hi in ((0, 500), (M - 500, M)):
         small = _gemm(torch, 1, Wt, xt[lo:hi].contiguous(), hi - lo)
         assert np.array_equal(small.view(np.uint32), big[lo:hi].view(np.uint32)), (lo, hi)
     assert np.array_equal(big.view(np.uint32), _gemm(torch, 1, Wt, xt, M).view(np.uint32))
