@@ -222,27 +222,28 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
   }
 }
 
-// Large form (whenever its grid has at least BG_MIN_WG workgroups; below
-// that the 128 x 128 form keeps more CUs busy): a workgroup of eight waves owns 256 weight
-// rows (16 packed blocks per k-step: 16 tiles, or 8 gate/up pairs) x 256
-// input rows and stages both operands through LDS in fragment order, so each
-// operand byte fetched from L2 feeds 16 MFMA tiles instead of 2.  The k-steps
-// (32 KB each) move global -> LDS with direct transfers (global_load_lds,
-// 16 bytes per lane at LDS base + 16 x lane) into a ring of four slots,
-// three steps ahead of the products: no staging registers, and each wave
-// waits (vmcnt) only for its own oldest step before the per-step barrier.  Wave (wn, wm) multiplies weight
-// blocks 8 wn .. 8 wn + 7 by input fragments 4 wm .. 4 wm + 3 (128 x 64
-// outputs) with the operand roles of gemm_tiled_kernel, accumulating the
-// k-steps in order, and hands each tile to the shared epilogue.  Workgroups
-// are numbered so that each XCD takes a contiguous run of tiles, grouped
-// eight input blocks deep, which keeps the operands the XCD's waves share in
-// its own L2.
+// Large form, taken whenever its grid has at least BG_MIN_WG workgroups
+// (below that the 128 x 128 form keeps more CUs busy).  A workgroup of eight
+// waves owns 256 weight rows (16 packed blocks per k-step: 16 tiles, or 8
+// gate/up pairs) x 256 input rows and stages both operands through LDS in
+// fragment order, so each operand byte fetched from L2 feeds 16 MFMA tiles
+// instead of 2.  The k-steps (32 KB each) move global -> LDS with direct
+// transfers (global_load_lds, 16 bytes per lane at LDS base + 16 x lane)
+// into a ring of four slots, three steps ahead of the products: no staging
+// registers, and each wave waits (vmcnt) only for its own oldest step before
+// the per-step barrier.  Wave (wn, wm) multiplies weight blocks
+// 8 wn .. 8 wn + 7 by input fragments 4 wm .. 4 wm + 3 (128 x 64 outputs)
+// with the operand roles of gemm_tiled_kernel, accumulating the k-steps in
+// order, and hands each tile to the shared epilogue.  Workgroups are
+// numbered so that each XCD takes a contiguous run of tiles, grouped eight
+// input blocks deep, which keeps the operands the XCD's waves share in its
+// own L2.
 constexpr int BG_THREADS = 512;
 constexpr int BG_ROWS = 256;      // input rows per workgroup
 constexpr int BG_BLK = 16;        // weight blocks per k-step per workgroup
 constexpr int BG_NBUF = 4;        // LDS stages in the ring (three in flight)
 constexpr int BG_GROUP = 8;       // input blocks per tile group
-constexpr int BG_MIN_WG = 96;    // smallest grid that takes this form
+constexpr int BG_MIN_WG = 96;     // smallest grid that takes this form
 
 __device__ tb_u32x4 bg_zero[64];  // source of the zero lanes outside the operands
 

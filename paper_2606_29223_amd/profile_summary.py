@@ -40,23 +40,48 @@ SHORT = {
 }
 
 
+def code_text(src: str) -> str:
+    """C/C++/HIP source with comments removed and whitespace runs collapsed:
+    what the compiler sees, so a comment edit leaves a measurement valid."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":                       # string or character literal
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def gemm_source_hash() -> str:
-    """Hash of the decode GEMM kernel source and of its argument struct."""
+    """Hash of the decode GEMM kernel code and of its argument struct."""
     h = hashlib.sha1()
-    h.update(open(os.path.join(PKG, "csrc", "gemm.hip"), "rb").read())
+    h.update(code_text(open(os.path.join(PKG, "csrc", "gemm.hip")).read()).encode())
     hdr = open(os.path.join(PKG, "csrc", "dex_kernels.h")).read()
     start = hdr.index("struct GemmArgs {")
-    h.update(hdr[start:hdr.index("};", start)].encode())
+    h.update(code_text(hdr[start:hdr.index("};", start)]).encode())
     return h.hexdigest()[:16]
 
 
 def csrc_source_hash() -> str:
-    """Hash of every kernel and engine source: whole-round traffic depends on
-    all of them."""
+    """Hash of every kernel and engine source's code (comments and spacing
+    aside): whole-round traffic depends on all of them."""
     h = hashlib.sha1()
     for f in sorted(glob.glob(os.path.join(PKG, "csrc", "*"))):
         h.update(os.path.basename(f).encode())
-        h.update(open(f, "rb").read())
+        h.update(code_text(open(f).read()).encode())
     return h.hexdigest()[:16]
 
 
