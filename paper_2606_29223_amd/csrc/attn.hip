@@ -918,8 +918,8 @@ __global__ __launch_bounds__(64 * G) __attribute__((amdgpu_waves_per_eu(2))) voi
   issue(0, 0);
   for (int j = 0; j < nblk; ++j) {
     const int slot = j & 1, k0 = j * KB;
-    __builtin_amdgcn_s_waitcnt(0x0F70);      // this wave's transfers of block j are done
-    __builtin_amdgcn_s_barrier();            // every wave's, and every wave is past block j - 1
+    lds_ring_step<0>();                      // block j has landed for every wave, and every
+                                             // wave is past block j - 1
     if (j + 1 < nblk) issue(j + 1, slot ^ 1);
     const uint4 *K = kl[slot];
     // S^T = K Q^T

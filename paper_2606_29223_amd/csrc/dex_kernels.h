@@ -19,6 +19,22 @@ __device__ __forceinline__ int qkv_col(int tile, int r16, int hd) {
 
 typedef uint16_t bf16;
 
+// Step of an LDS ring filled by direct global -> LDS transfers
+// (global_load_lds): wait until at most VMCNT of this wave's vector-memory
+// operations are outstanding (the oldest transfers have landed in LDS), then
+// meet the workgroup's other waves.  Unlike __syncthreads() it does not wait
+// for the younger transfers still in flight.  The empty asm statements emit
+// nothing; they keep the compiler from moving any memory access across the
+// wait and the barrier.
+template <int VMCNT>
+__device__ __forceinline__ void lds_ring_step() {
+  static_assert(VMCNT >= 0 && VMCNT < 16, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | VMCNT);   // lgkmcnt, expcnt: no wait
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Sampling-mode Gumbel noise of token v for the slot of sequence `seq` at
 // position `pos` (the definition is stated with dex_debug_gumbel in dex.h).
 __device__ __forceinline__ unsigned long long sm64_mix(unsigned long long z) {

@@ -309,10 +309,9 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
     // (up to two) younger steps are outstanding; the barrier makes every
     // wave's done, and tells that all waves have finished step st - 1
     const int younger = min(nsteps - 1 - st, BG_NBUF - 2);
-    if (younger >= 2) __builtin_amdgcn_s_waitcnt(0x0F70 | 8);
-    else if (younger == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | 4);
-    else __builtin_amdgcn_s_waitcnt(0x0F70);
-    __builtin_amdgcn_s_barrier();
+    if (younger >= 2) lds_ring_step<8>();
+    else if (younger == 1) lds_ring_step<4>();
+    else lds_ring_step<0>();
     if (st + BG_NBUF - 1 < nsteps) issue(st + BG_NBUF - 1, (st + BG_NBUF - 1) % BG_NBUF);
     const int slot = st % BG_NBUF;
     tb_u32x4 w[WB], x[WF];
