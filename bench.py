@@ -99,7 +99,7 @@ def cpu_baseline(cfg, weights, prompts, budget_s, temperature=0.0, seed=0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+        print(json.dumps({"error": "the decode step runs on one GPU (no multi-GPU path); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
