@@ -69,10 +69,11 @@ def test_tiled_prefill_gemm_matches_float64(N, K, M):
     assert np.array_equal(y.view(np.uint32), _gemm(torch, 1, Wt, xt, M).view(np.uint32))
 
 
-@pytest.mark.parametrize("N,K,M", [(6144, 4096, 2100), (2064, 14336, 3000), (1552, 768, 4000)])
+@pytest.mark.parametrize("N,K,M", [(6144, 4096, 2100), (2064, 14336, 3000), (1552, 776, 4000)])
 def test_large_prefill_gemm_matches_the_small_tiles(N, K, M):
     """A grid of 96 or more 256 x 256 workgroups (here 216, 108 and 112, with
-    ragged last blocks in M and N) takes the LDS-staged kernel.  It feeds
+    ragged last blocks in M and N, and a last k-step only a quarter inside
+    K = 776) takes the LDS-staged kernel.  It feeds
     every MFMA tile the same operands in the same k-step order as the
     128 x 128 kernel, which 500-row launches of the same rows take (at most
     48 such workgroups), so each row's bits are equal; and float64 parity
