@@ -106,12 +106,15 @@ def test_kv_collapse_full_size(llama):
     assert checked >= 3
 
 
-def test_oracle_sampled_positions_full_size(llama):
+@pytest.mark.parametrize("name", [C3, C4])
+def test_oracle_sampled_positions_full_size(llama, name):
     """The float64 oracle re-scores sampled positions of the GPU's sequence:
     the committed token is its argmax (or a near tie) and every explored
-    depth's exit logits agree within 2e-2 (max relative)."""
+    depth's exit logits agree within 2e-2 (max relative) -- four depths at
+    width 4, sixteen at width 16."""
     torch = torch_cuda()
-    cfg, w, dev_w = llama
+    _, w, dev_w = llama
+    cfg = configs.get(name)
     P = cfg["prompt_len"]
     T = 12
     prompt = gen.prompts(cfg)
