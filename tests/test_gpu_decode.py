@@ -268,6 +268,28 @@ def test_small_bf16_explored_sets(X, W, decs):
         _replay(rounds, len(X), W, decs, P + T, toks[b][0], P, seq=b)
 
 
+def test_small_bf16_lossless_over_seeds():
+    """Losslessness over more seeded prompts: six prompt sets of three
+    sequences (prompt lengths 24 to 109), each decoded by DEX under one of
+    three explored-set / width-cap / DECS settings (two sets each), equal
+    plain AR token for token."""
+    torch_cuda()
+    cfg = configs.get(SMALL)
+    T = 40
+    cases = [([3, 6, 9, 12], 4, 1), ([2, 5, 8, 12], 3, 1), ([4, 12], 0, 0)]
+    for seed in range(6):
+        P = 24 + 17 * seed
+        prompts = np.stack([gen.tokens(gen.mix64(9000 + 10 * seed + b), P, cfg["vocab"]) for b in range(3)])
+        ar_dec = decoder(SMALL, explored=[cfg["n_layers"]], width_cap=1, batch=3, max_context=P + T)
+        ar_toks, _ = _run(ar_dec, prompts, T, collapse=False)
+        ar_dec.close()
+        X, W, decs = cases[seed % len(cases)]
+        dec = decoder(SMALL, explored=X, width_cap=W, decs=decs, batch=3, max_context=P + T)
+        toks, _ = _run(dec, prompts, T, collapse=False)
+        dec.close()
+        assert np.array_equal(toks, ar_toks), (seed, X, W, decs)
+
+
 @pytest.mark.parametrize("P", [1, 45, 97])
 def test_small_bf16_prefill_ragged_prompts(P):
     """Prompt lengths that are not a multiple of the 32-query / 64-key tiles
