@@ -232,23 +232,28 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 // order (lanes over head dimensions) and the wave sums are added in wave
 // order; the statistics take one fixed reduction.  The arithmetic depends
 // only on the row's split count, never on the other rows of the launch.
+// DW head dimensions per workgroup (blockIdx.z picks the slice): each
+// dimension's sum is computed the same way whatever the slicing, so a
+// launch with few rows splits a head over two workgroups for more latency
+// hiding, and the bits do not change.
 #ifndef CMB_WAVES
 #define CMB_WAVES 4
 #endif
-template <typename T, int HD>
+template <typename T, int HD, int DW>
 __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) {
-  constexpr int DPL = HD >= 64 ? HD / 64 : 1;
+  constexpr int DPL = DW >= 64 ? DW / 64 : 1;
   constexpr int CH = 16;                       // splits per value chunk
   constexpr int NT = 64 * CMB_WAVES;
   extern __shared__ float ws[];                // [jmax] split weights
-  __shared__ float red[CMB_WAVES][HD];         // per-wave weighted sums
+  __shared__ float red[CMB_WAVES][DW];         // per-wave weighted sums
   __shared__ float sred[2][CMB_WAVES];         // per-wave max and denominator
   const int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, s = tid >> 6;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
   const int nmine = nsplit > s ? (nsplit - s + CMB_WAVES - 1) / CMB_WAVES : 0;
   const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (HD + 2);
-  const int d0 = lane * DPL;
-  const bool dok = d0 < HD;
+  const int dl = lane * DPL;                   // this lane's first dimension in the slice
+  const int d0 = blockIdx.z * DW + dl;
+  const bool dok = dl < DW;
   // the split values do not depend on the statistics: the first chunk is
   // requested before them, each next chunk before the current one is summed
   float va[CH][DPL], vb[CH][DPL];
@@ -303,16 +308,16 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   }
   if (dok) {
 #pragma unroll
-    for (int q = 0; q < DPL; ++q) red[s][d0 + q] = o[q];
+    for (int q = 0; q < DPL; ++q) red[s][dl + q] = o[q];
   }
   __syncthreads();
   if (s != 0 || !dok) return;
   T *out = (T *)a.out + (size_t)r * a.ld_out + h * HD + d0;
 #pragma unroll
   for (int q = 0; q < DPL; ++q) {
-    float v = red[0][d0 + q];
+    float v = red[0][dl + q];
 #pragma unroll
-    for (int w = 1; w < CMB_WAVES; ++w) v += red[w][d0 + q];
+    for (int w = 1; w < CMB_WAVES; ++w) v += red[w][dl + q];
     v = v / lsum;
     if constexpr (sizeof(T) == 2) {
       uint32_t u = __float_as_uint(v);
@@ -336,11 +341,20 @@ static hipError_t launch_attn_t(const AttnArgs &a, dim3 grid, hipStream_t s) {
 }
 
 template <typename T>
-static hipError_t launch_comb_t(const CombineArgs &a, dim3 grid, hipStream_t s) {
+static hipError_t launch_comb_t(const CombineArgs &a, int rows, hipStream_t s) {
+  const size_t smem = (size_t)a.jmax * 4;
+  const dim3 block(64 * CMB_WAVES);
   switch (a.head_dim) {
-    case 32: hipLaunchKernelGGL((combine_kernel<T, 32>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
-    case 64: hipLaunchKernelGGL((combine_kernel<T, 64>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
-    case 128: hipLaunchKernelGGL((combine_kernel<T, 128>), grid, dim3(64 * CMB_WAVES), a.jmax * 4, s, a); break;
+    case 32: hipLaunchKernelGGL((combine_kernel<T, 32, 32>), dim3(rows, a.n_heads), block, smem, s, a); break;
+    case 64: hipLaunchKernelGGL((combine_kernel<T, 64, 64>), dim3(rows, a.n_heads), block, smem, s, a); break;
+    case 128:
+      // up to 512 (row, head) pairs: half a head per workgroup (latency-bound
+      // launches); beyond, a whole head (bandwidth-bound, fewer statistics reads)
+      if ((size_t)rows * a.n_heads <= 512)
+        hipLaunchKernelGGL((combine_kernel<T, 128, 64>), dim3(rows, a.n_heads, 2), block, smem, s, a);
+      else
+        hipLaunchKernelGGL((combine_kernel<T, 128, 128>), dim3(rows, a.n_heads, 1), block, smem, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -349,8 +363,7 @@ static hipError_t launch_comb_t(const CombineArgs &a, dim3 grid, hipStream_t s) 
 hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (a.jmax > ATT_MAX_SPLITS) return hipErrorInvalidValue;
-  dim3 grid(rows, a.n_heads);
-  return dtype == 1 ? launch_comb_t<bf16>(a, grid, s) : launch_comb_t<float>(a, grid, s);
+  return dtype == 1 ? launch_comb_t<bf16>(a, rows, s) : launch_comb_t<float>(a, rows, s);
 }
 
 
