@@ -361,14 +361,17 @@ def test_large_prompt_batch_prefill_matches_batch_one():
     assert t2 == t1
 
 
-@pytest.mark.parametrize("P", [1, 45, 97, 300])
+@pytest.mark.parametrize("P", [1, 45, 97, 300, 3100])
 def test_gqa128_prefill_ragged_prompts(P):
     """The 32-layer model's attention shape (head_dim 128, four query heads
     per kv head) on a 2-layer model small enough for the float64 oracle, with
     prompt lengths that are not multiples of the 32-query / 64-key blocks of
     the prompt attention (and the one-token prompt), at batch 2: y_0 and the
     next tokens follow the oracle (near ties aside) and every decoded row's
-    exit logits agree within 2e-2 (max relative)."""
+    exit logits agree within 2e-2 (max relative).  At 2 x 3100 prompt rows
+    all four prompt GEMMs (QKV with RoPE and the cache write, O and down with
+    the residual, gate/up with SwiGLU) take the 256 x 256 LDS-staged form
+    (150, 100, 400 and 100 workgroups)."""
     torch = torch_cuda()
     from paper_2606_29223_amd import dexlib
     cfg = configs.scaled_down(configs.get("llama-32L-d4096-x8-w4"), n_layers=2, d_model=1024, d_ffn=2048,
