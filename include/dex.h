@@ -34,8 +34,13 @@
  *   - All device work is enqueued on config.hip_stream (NULL = the default
  *     stream).  dex_prefill and dex_step synchronise that stream before
  *     returning host results.  A context is not thread-safe.
- *   - After any failure inside dex_prefill or dex_step the context is
- *     poisoned: later calls return DEX_E_STATE.
+ *   - Argument errors (DEX_E_INVAL), a prefill that could not allocate its
+ *     scratch (DEX_E_NOMEM) and "every sequence is full" (DEX_E_CAPACITY
+ *     before any work) leave the context as it was.  Any other failure
+ *     inside an entry point -- a failed HIP call, a lattice capacity
+ *     overflow found after the round's planning began, a host/device commit
+ *     mismatch -- poisons it: later dex_prefill / dex_step calls return
+ *     DEX_E_STATE; dex_destroy still frees everything.
  */
 #ifndef DEX_H
 #define DEX_H

@@ -140,11 +140,14 @@ struct dex_ctx {
 
 namespace {
 
+// A failed HIP call leaves device work of the call half done: the context
+// is poisoned.
 #define HIPCHK(expr)                                                          \
   do {                                                                        \
     hipError_t e_ = (expr);                                                   \
     if (e_ != hipSuccess) {                                                   \
       ctx->err = std::string(#expr) + ": " + hipGetErrorString(e_);           \
+      ctx->poisoned = true;                                                   \
       return DEX_E_HIP;                                                       \
     }                                                                         \
   } while (0)
@@ -383,7 +386,6 @@ dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_la
   return DEX_OK;
 }
 
-// exit head over M rows whose final state sits in (src_h, src_part)[row_src[m]]
 // Rows [r0, r0 + M) of the exit buffers from their source states, with the
 // next norm's input g * h.
 dex_status exit_prep(dex_ctx *ctx, int r0, int M, const int *row_src, const float *src_h, const float *src_part,
@@ -472,8 +474,17 @@ dex_status run_exit(dex_ctx *ctx, int M, const int *row_src, const float *src_h,
   return DEX_OK;
 }
 
+// Argument errors and a full context leave the state as it was; any other
+// failure poisons it.
 dex_status fail(dex_ctx *ctx, dex_status s) {
   if (s != DEX_OK && s != DEX_E_INVAL && s != DEX_E_CAPACITY) ctx->poisoned = true;
+  return s;
+}
+
+// A failure after the round's planning has changed the lattice.
+dex_status fail_mid_round(dex_ctx *ctx, const char *msg, dex_status s) {
+  ctx->err = msg;
+  ctx->poisoned = true;
   return s;
 }
 
@@ -756,7 +767,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     dfree(ctx, h); dfree(ctx, part); dfree(ctx, xb); dfree(ctx, q); dfree(ctx, att); dfree(ctx, act);
     dfree(ctx, apart); dfree(ctx, tab);
   };
-  if (st != DEX_OK) { cleanup(); return fail(ctx, st); }
+  if (st != DEX_OK) { cleanup(); return st; }   // nothing changed yet: not poisoned
 
   // row tables: rows ordered (seq, position)
   std::vector<int> host(tab_ints, 0);
@@ -926,7 +937,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
       if (it.kind == 0) {
         rows.push_back({si, it.slot, s.slots[it.slot].c});
       } else {
-        if ((int)s.slots.size() >= ctx->S) { ctx->err = "lattice slot capacity exceeded"; return fail(ctx, DEX_E_CAPACITY); }
+        if ((int)s.slots.size() >= ctx->S) return fail_mid_round(ctx, "lattice slot capacity exceeded", DEX_E_CAPACITY);
         Slot ns;
         ns.x = s.slots[it.slot].u[it.f];
         ns.pos = s.slots[it.slot].pos + 1;
@@ -946,7 +957,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     return a.seq < b.seq;
   });
   const int R = (int)rows.size();
-  if (R > ctx->R_max) { ctx->err = "round rows exceed capacity"; return fail(ctx, DEX_E_CAPACITY); }
+  if (R > ctx->R_max) return fail_mid_round(ctx, "round rows exceed capacity", DEX_E_CAPACITY);
 
   // ------------------------------------------------------- row tables
   int *T = ctx->tab_host;
@@ -973,7 +984,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     t_nc[r] = (int)s.committed.size() - 1;
     t_coff[r] = chain_used;
     std::vector<int> anc = ancestors(s, rw.slot);
-    if ((int)anc.size() + 1 > ctx->CH_MAX) { ctx->err = "lattice chain too deep"; return fail(ctx, DEX_E_CAPACITY); }
+    if ((int)anc.size() + 1 > ctx->CH_MAX) return fail_mid_round(ctx, "lattice chain too deep", DEX_E_CAPACITY);
     for (int a : anc) t_chain[chain_used++] = slot_entry(ctx, s, a);
     t_chain[chain_used++] = slot_entry(ctx, s, rw.slot);
     // DECS mask: tokens proposed by shallower nodes of this slot chain,
@@ -1013,7 +1024,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     }
   }
   const size_t tab_ints = (size_t)(t_rcommit - T) + R;
-  if (tab_ints > ctx->tab_cap) { ctx->err = "row table overflow"; return fail(ctx, DEX_E_CAPACITY); }
+  if (tab_ints > ctx->tab_cap) return fail_mid_round(ctx, "row table overflow", DEX_E_CAPACITY);
   HIPCHK(hipMemcpyAsync(ctx->tab_dev, T, tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
   const int *D = ctx->tab_dev;
   auto dptr = [&](const int *hp) { return D + (hp - T); };
@@ -1124,10 +1135,8 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     int kh = N - 1;
     for (int j = 0; j < N - 1; ++j)
       if (A.u[j] == A.u[N - 1]) { kh = j; break; }
-    if (A.c != N || y != A.u[N - 1] || kstar != kh) {
-      ctx->err = "commit mismatch between device and host lattice";
-      return fail(ctx, DEX_E_HIP);
-    }
+    if (A.c != N || y != A.u[N - 1] || kstar != kh)
+      return fail_mid_round(ctx, "commit mismatch between device and host lattice", DEX_E_HIP);
     committed_out[si] = y;
     if (info) info->kstar[si] = kstar;
     s.committed.push_back(y);
@@ -1261,9 +1270,16 @@ dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t r
   if (cls != 3 && cls != 4 && cls != 5 && cls != 6) { ctx->err = "only o-proj, gate/up, down, lm-head"; return DEX_E_INVAL; }
   if (!ctx->prefilled) { ctx->err = "time_kernel needs a prefilled context"; return DEX_E_STATE; }
   const int d = ctx->d, H = ctx->H, hd = ctx->hd, F = ctx->F;
-  hipEvent_t e0, e1;
-  HIPCHK(hipEventCreate(&e0));
-  HIPCHK(hipEventCreate(&e1));
+  struct Events {
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    ~Events() {
+      if (e0) (void)hipEventDestroy(e0);
+      if (e1) (void)hipEventDestroy(e1);
+    }
+  } ev;
+  HIPCHK(hipEventCreate(&ev.e0));
+  HIPCHK(hipEventCreate(&ev.e1));
+  hipEvent_t e0 = ev.e0, e1 = ev.e1;
   double bytes = 0.0;
   auto launch = [&](int rep) -> hipError_t {
     const int l = rep % ctx->L;
@@ -1303,8 +1319,6 @@ dex_status dex_debug_time_kernel(dex_ctx *ctx, int32_t cls, int32_t M, int32_t r
   HIPCHK(hipEventSynchronize(e1));
   float ms = 0.f;
   HIPCHK(hipEventElapsedTime(&ms, e0, e1));
-  (void)hipEventDestroy(e0);
-  (void)hipEventDestroy(e1);
   *avg_us = (double)ms * 1e3 / reps;
   *bytes_per_launch = bytes;
   return DEX_OK;
