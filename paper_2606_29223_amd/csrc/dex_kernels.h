@@ -82,6 +82,9 @@ struct GemmArgs {
   const float *part;
   int n_part;
   float inv_d, eps;
+  // Prompt GEMMs (launch_gemm_tiled): the same scales precomputed per row by
+  // launch_row_scale, required there whenever part is set.
+  const float *row_rsc;
   // PLAIN / QKV: float output [M][ld_out]
   float *out;
   int ld_out;
@@ -173,9 +176,12 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipS
 // workgroup) with the QKV / RESID / SWIGLU / PLAIN epilogues.  Requires N a
 // multiple of 16, K a multiple of 8, 16-byte aligned rows and no boundary
 // rows (gemm_tiled_supported); launch_gemm_tiled returns hipErrorInvalidValue
-// otherwise.
+// otherwise.  A normed GEMM takes its row scales from row_rsc.
 bool gemm_tiled_supported(int epi, const GemmArgs &a);
 hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s);
+// out[m] = 1 / sqrt(sum(part[m][0..n_part)) * inv_d + eps), m < M: the RMSNorm
+// scales launch_gemm_tiled reads, summed in index order.
+hipError_t launch_row_scale(const float *part, int n_part, int M, float inv_d, float eps, float *out, hipStream_t s);
 hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s);
 hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s);
 

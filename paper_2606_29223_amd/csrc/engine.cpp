@@ -746,7 +746,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
   chunk = (chunk / grp_rows) * grp_rows;
   if (chunk == 0) chunk = grp_rows;
 
-  float *h = nullptr, *part = nullptr, *q = nullptr, *apart = nullptr;
+  float *h = nullptr, *part = nullptr, *q = nullptr, *apart = nullptr, *rsc = nullptr;
   void *xb = nullptr, *att = nullptr, *act = nullptr;
   int *tab = nullptr;
   dex_status st = DEX_OK;
@@ -759,13 +759,14 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
   A((void **)&q, M * H * hd * 4);
   A(&att, M * H * hd * es);
   A(&act, M * ctx->F * es);
+  A((void **)&rsc, M * 4);
   if (!mfma_prefill) A((void **)&apart, chunk * per_row);
   const size_t n_groups_total = (size_t)B * ((P + grp_rows - 1) / grp_rows);
   const size_t tab_ints = M * 8 + n_groups_total * 4 + 6 * B + 64;
   A((void **)&tab, tab_ints * 4);
   auto cleanup = [&]() {
     dfree(ctx, h); dfree(ctx, part); dfree(ctx, xb); dfree(ctx, q); dfree(ctx, att); dfree(ctx, act);
-    dfree(ctx, apart); dfree(ctx, tab);
+    dfree(ctx, apart); dfree(ctx, tab); dfree(ctx, rsc);
   };
   if (st != DEX_OK) { cleanup(); return st; }   // nothing changed yet: not poisoned
 
@@ -822,9 +823,20 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
     HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
   }
   const size_t layer_kv = (size_t)B * ctx->Hkv * ctx->E * hd * es;
-  // many prompt rows: the M-tiled kernel (bf16); the decode kernel otherwise
+  // many prompt rows: the M-tiled kernel (bf16; a normed GEMM first gets
+  // its row scales); the decode kernel otherwise
   auto prefill_gemm = [&](int epi, const GemmArgs &a) -> hipError_t {
-    if (ctx->dtype == DEX_BF16 && a.M > 64 && gemm_tiled_supported(epi, a)) return launch_gemm_tiled(epi, a, ctx->stream);
+    if (ctx->dtype == DEX_BF16 && a.M > 64) {
+      GemmArgs t = a;
+      t.row_rsc = a.part != nullptr ? rsc : nullptr;
+      if (gemm_tiled_supported(epi, t)) {
+        if (t.row_rsc != nullptr) {
+          const hipError_t e = launch_row_scale(a.part, a.n_part, a.M, a.inv_d, a.eps, rsc, ctx->stream);
+          if (e != hipSuccess) return e;
+        }
+        return launch_gemm_tiled(epi, t, ctx->stream);
+      }
+    }
     return launch_gemm(ctx->dtype, epi, a, 1, ctx->stream);
   };
   for (int l = 0; l < ctx->L; ++l) {

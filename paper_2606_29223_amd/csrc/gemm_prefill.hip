@@ -19,7 +19,9 @@
 // the key/value cache write; residual add with the next norm's input and its
 // sum-of-squares partials; SwiGLU), applied to the accumulators in registers:
 // lane (g, r) of a tile holds output rows 4g..4g+3 of input row r, so every
-// store covers four consecutive columns.
+// store covers four consecutive columns.  The row scales of a normed GEMM
+// are computed once beforehand (row_scale_kernel) rather than by each of
+// its column blocks.
 #include "dex_kernels.h"
 
 namespace dex {
@@ -42,11 +44,38 @@ __device__ __forceinline__ uint2 tb_pack4(float a, float b, float c, float d) {
   return make_uint2(tb_f2bf(a) | (tb_f2bf(b) << 16), tb_f2bf(c) | (tb_f2bf(d) << 16));
 }
 
+// Sum of a row's n sum-of-squares partials in index order.  The loads go out
+// 32 at a time, so that a batch waits for one memory latency rather than
+// one per partial; the padding terms are +0, which leaves the sum (>= +0)
+// unchanged.
+__device__ __forceinline__ float tb_part_sum(const float *p, int n) {
+  float ss = 0.f;
+  for (int q0 = 0; q0 < n; q0 += 32) {
+    float v[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) v[i] = q0 + i < n ? p[q0 + i] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) ss += v[i];
+  }
+  return ss;
+}
+
+// RMSNorm reciprocal scale of every prompt row, once per normed GEMM (each
+// of a GEMM's column blocks would otherwise reduce the row's partials
+// again): one thread per row.
+__global__ __launch_bounds__(256) void row_scale_kernel(const float *part, int n_part, int M, float inv_d, float eps,
+                                                        float *out) {
+  const int m = blockIdx.x * 256 + threadIdx.x;
+  if (m >= M) return;
+  const float ss = tb_part_sum(part + (size_t)m * n_part, n_part);
+  out[m] = 1.0f / sqrtf(ss * inv_d + eps);
+}
+
 // Epilogue of one 16 x 16 output tile held by a wave: lane (g, r) holds
 // output columns tile*16 + 4g .. +3 of input row m (ok: m < M).  Every lane
-// of the wave calls it (the QKV and RESID forms exchange values across
-// lanes).  acc[0] is the tile (SwiGLU: the gate tile, acc[1] the up tile),
-// rsc the row's RMSNorm scale.
+// of the wave calls it (the RESID form exchanges values across lanes).
+// acc[0] is the tile (SwiGLU: the gate tile, acc[1] the up tile), rsc the
+// row's RMSNorm scale.  The QKV epilogue is tb_qkv_block.
 template <int EPI, int NT>
 __device__ __forceinline__ void tb_epilogue(const GemmArgs &a, int tile, int m, bool ok, const tb_f32x4 (&acc)[NT],
                                             float rsc, int grp) {
@@ -54,37 +83,6 @@ __device__ __forceinline__ void tb_epilogue(const GemmArgs &a, int tile, int m, 
     if (ok) {
       float *o = a.out + (size_t)m * a.ld_out + tile * 16 + grp * 4;
       *(float4 *)o = make_float4(acc[0][0], acc[0][1], acc[0][2], acc[0][3]);
-    }
-  } else if constexpr (EPI == EPI_QKV) {
-    const int hd = a.head_dim;
-    const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
-    const int col0 = qkv_col(tile, 0, hd);
-    const int head_col = col0 - col0 % hd;   // first column of this head
-    const int j = tile % (hd / 16);
-    const bool lo = grp < 2;                 // rows 0..7: dims i; rows 8..15: dims i + hd/2
-    const int i0 = 8 * j + (grp & 1) * 4;    // RoPE pair index of this lane's first row
-    float y[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float v = acc[0][i] * rsc;
-      const float partner = __shfl_xor(v, 32, 64);
-      y[i] = v;
-      if (ok && head_col < nq + nk) {        // q or k: rotate the pair
-        const float2 cs = a.rope[(size_t)a.row_pos[m] * (hd / 2) + i0 + i];
-        y[i] = lo ? v * cs.x - partner * cs.y : v * cs.x + partner * cs.y;
-      }
-    }
-    if (ok) {
-      const int dim0 = (lo ? 0 : hd / 2) + i0;
-      if (head_col < nq) {
-        *(float4 *)(a.out + (size_t)m * a.ld_out + head_col + dim0) = make_float4(y[0], y[1], y[2], y[3]);
-      } else {
-        const bool isk = head_col < nq + nk;
-        const int g = (isk ? head_col - nq : head_col - nq - nk) / hd;
-        uint16_t *cache = (uint16_t *)(isk ? a.kc : a.vc);
-        const size_t base = (((size_t)a.row_seq[m] * a.n_kv_heads + g) * a.kv_entries + a.row_entry[m]) * hd;
-        *(uint2 *)(cache + base + dim0) = tb_pack4(y[0], y[1], y[2], y[3]);
-      }
     }
   } else if constexpr (EPI == EPI_RESID) {
     const int n0 = tile * 16 + grp * 4;
@@ -118,6 +116,88 @@ __device__ __forceinline__ void tb_epilogue(const GemmArgs &a, int tile, int m, 
         o[i] = gt / (1.0f + expf(-gt)) * up;
       }
       *(uint2 *)((uint16_t *)a.act + (size_t)m * a.ld_act + tile * 16 + grp * 4) = tb_pack4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+// QKV epilogue of the tiles T0 .. T0 + NTL - 1 (consecutive) over NF input
+// fragments (lane (g, r) of fragment f: input row mbase + 16 f + r): RMSNorm
+// scale, RoPE on the query and key columns (the tile's rows 0..7 hold
+// dimensions i of a head, rows 8..15 dimensions i + hd/2: the partner of a
+// value sits 32 lanes away), queries to out (fp32), keys and values to the
+// cache entry of the row.  The row-table loads, and the RoPE-table loads of
+// four tiles at a time, are issued before the stores they feed, so that
+// they are not held behind stores to memory the compiler cannot tell apart
+// from the tables.
+template <int NTL, int NF, typename Acc>
+__device__ __forceinline__ void tb_qkv_block(const GemmArgs &a, int T0, int mbase, const float (&rsc)[NF], int r16,
+                                             int grp, Acc acc) {
+  const int hd = a.head_dim;
+  const int nq = a.n_heads * hd, nk = a.n_kv_heads * hd;
+  const int n_tiles = a.N / 16;
+  const bool lo = grp < 2;
+  int pos[NF], seq[NF], ent[NF];
+  bool ok[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int m = mbase + f * 16 + r16;
+    ok[f] = m < a.M;
+    const int mm = ok[f] ? m : 0;
+    pos[f] = a.row_pos[mm];
+    seq[f] = a.row_seq[mm];
+    ent[f] = a.row_entry[mm];
+  }
+  constexpr int CH = NTL < 4 ? NTL : 4;     // tiles per batch of RoPE loads
+  static_assert(NTL % CH == 0, "tile batches");
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+#pragma unroll
+    for (int p0 = 0; p0 < NTL; p0 += CH) {
+      float4 cs[CH][2];                        // (cos, sin) of the lane's four pairs
+#pragma unroll
+      for (int q = 0; q < CH; ++q) {
+        const int p = p0 + q, tile = T0 + p;
+        const int col0 = qkv_col(tile, 0, hd), head_col = col0 - col0 % hd;
+        const int i0 = 8 * (tile % (hd / 16)) + (grp & 1) * 4;
+        if (tile < n_tiles && head_col < nq + nk) {
+          const float4 *rp = (const float4 *)(a.rope + (size_t)pos[f] * (hd / 2) + i0);
+          cs[q][0] = rp[0];
+          cs[q][1] = rp[1];
+        } else {
+          cs[q][0] = cs[q][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < CH; ++q) {
+        const int p = p0 + q, tile = T0 + p;
+        if (tile >= n_tiles) continue;         // uniform across the wave
+        const int col0 = qkv_col(tile, 0, hd), head_col = col0 - col0 % hd;
+        const int i0 = 8 * (tile % (hd / 16)) + (grp & 1) * 4;
+        const tb_f32x4 t = acc(p, f);
+        const float c[4] = {cs[q][0].x, cs[q][0].z, cs[q][1].x, cs[q][1].z};
+        const float sn[4] = {cs[q][0].y, cs[q][0].w, cs[q][1].y, cs[q][1].w};
+        float y[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v = t[i] * rsc[f];
+          const float partner = __shfl_xor(v, 32, 64);
+          y[i] = v;
+          if (ok[f] && head_col < nq + nk)     // q or k: rotate the pair
+            y[i] = lo ? v * c[i] - partner * sn[i] : v * c[i] + partner * sn[i];
+        }
+        if (!ok[f]) continue;
+        const int dim0 = (lo ? 0 : hd / 2) + i0;
+        if (head_col < nq) {
+          *(float4 *)(a.out + (size_t)(mbase + f * 16 + r16) * a.ld_out + head_col + dim0) =
+              make_float4(y[0], y[1], y[2], y[3]);
+        } else {
+          const bool isk = head_col < nq + nk;
+          const int g = (isk ? head_col - nq : head_col - nq - nk) / hd;
+          uint16_t *cache = (uint16_t *)(isk ? a.kc : a.vc);
+          const size_t base = (((size_t)seq[f] * a.n_kv_heads + g) * a.kv_entries + ent[f]) * hd;
+          *(uint2 *)(cache + base + dim0) = tb_pack4(y[0], y[1], y[2], y[3]);
+        }
+      }
     }
   }
 }
@@ -193,31 +273,26 @@ __global__ __launch_bounds__(TB_THREADS) void gemm_tiled_kernel(GemmArgs a) {
   // RMSNorm scale of each input row (lane j sums the partials of row
   // m_base + j in order), then handed to the lanes holding that row
   float rsc[TB_MF];
-  if (a.part != nullptr) {
-    const int m = m_base + lane;
-    float ss = 0.f;
-    if (m < a.M) {
-      const float *p = a.part + (size_t)m * a.n_part;
-      for (int t = 0; t < a.n_part; ++t) ss += p[t];
-    }
-    const float r = 1.0f / sqrtf(ss * a.inv_d + a.eps);
 #pragma unroll
-    for (int f = 0; f < TB_MF; ++f) rsc[f] = __shfl(r, f * 16 + r16, 64);
-  } else {
-#pragma unroll
-    for (int f = 0; f < TB_MF; ++f) rsc[f] = 1.f;
+  for (int f = 0; f < TB_MF; ++f) {
+    const int m = m_base + f * 16 + r16;
+    rsc[f] = (a.row_rsc != nullptr && m < a.M) ? a.row_rsc[m] : 1.f;
   }
 
+  if constexpr (EPI == EPI_QKV) {
+    tb_qkv_block<TN, TB_MF>(a, tile0, m_base, rsc, r16, grp, [&](int t, int f) { return acc[t][0][f]; });
+  } else {
 #pragma unroll
-  for (int t = 0; t < TN; ++t) {
-    if (!tok[t]) continue;                    // uniform across the wave
+    for (int t = 0; t < TN; ++t) {
+      if (!tok[t]) continue;                  // uniform across the wave
 #pragma unroll
-    for (int f = 0; f < TB_MF; ++f) {
-      const int m = m_base + f * 16 + r16;
-      tb_f32x4 at[NT];
+      for (int f = 0; f < TB_MF; ++f) {
+        const int m = m_base + f * 16 + r16;
+        tb_f32x4 at[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) at[nt] = acc[t][nt][f];
-      tb_epilogue<EPI, NT>(a, tile0 + t, m, m < a.M, at, rsc[f], grp);
+        for (int nt = 0; nt < NT; ++nt) at[nt] = acc[t][nt][f];
+        tb_epilogue<EPI, NT>(a, tile0 + t, m, m < a.M, at, rsc[f], grp);
+      }
     }
   }
 }
@@ -279,8 +354,6 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
 #pragma unroll
     for (int f = 0; f < WF; ++f) acc[jb][f] = tb_f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // one k-step into slot `slot`: wave w moves blocks w, w + 8 (weights) and
-  // w + 16, w + 24 (input fragments), 1 KB each, global -> LDS
   // one k-step into slot `slot`: wave w moves weight blocks w, w + 8 and
   // input fragments w, w + 8 (1 KB each) global -> LDS, one instruction per
   // block; lanes outside the operands read zeros.  The source is chosen by
@@ -330,31 +403,26 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
   // RMSNorm scale of each input row of the wave (lane j sums the partials of
   // row m0 + 64 wm + j in order), handed to the lanes holding that row
   float rsc[WF];
-  if (a.part != nullptr) {
-    const int m = m0 + wm * 64 + lane;
-    float ss = 0.f;
-    if (m < a.M) {
-      const float *p = a.part + (size_t)m * a.n_part;
-      for (int q = 0; q < a.n_part; ++q) ss += p[q];
-    }
-    const float r = 1.0f / sqrtf(ss * a.inv_d + a.eps);
 #pragma unroll
-    for (int f = 0; f < WF; ++f) rsc[f] = __shfl(r, f * 16 + r16, 64);
+  for (int f = 0; f < WF; ++f) {
+    const int m = m0 + wm * 64 + f * 16 + r16;
+    rsc[f] = (a.row_rsc != nullptr && m < a.M) ? a.row_rsc[m] : 1.f;
+  }
+  if constexpr (EPI == EPI_QKV) {
+    tb_qkv_block<WB, WF>(a, tile0 + wn * WB, m0 + wm * 64, rsc, r16, grp, [&](int p, int f) { return acc[p][f]; });
   } else {
 #pragma unroll
-    for (int f = 0; f < WF; ++f) rsc[f] = 1.f;
-  }
+    for (int p = 0; p < WB / NT; ++p) {
+      const int tile = tile0 + wn * (WB / NT) + p;
+      if (tile >= n_tiles) continue;          // uniform across the wave
 #pragma unroll
-  for (int p = 0; p < WB / NT; ++p) {
-    const int tile = tile0 + wn * (WB / NT) + p;
-    if (tile >= n_tiles) continue;            // uniform across the wave
+      for (int f = 0; f < WF; ++f) {
+        const int m = m0 + wm * 64 + f * 16 + r16;
+        tb_f32x4 at[NT];
 #pragma unroll
-    for (int f = 0; f < WF; ++f) {
-      const int m = m0 + wm * 64 + f * 16 + r16;
-      tb_f32x4 at[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) at[nt] = acc[p * NT + nt][f];
-      tb_epilogue<EPI, NT>(a, tile, m, m < a.M, at, rsc[f], grp);
+        for (int nt = 0; nt < NT; ++nt) at[nt] = acc[p * NT + nt][f];
+        tb_epilogue<EPI, NT>(a, tile, m, m < a.M, at, rsc[f], grp);
+      }
     }
   }
 }
@@ -363,6 +431,7 @@ __global__ __launch_bounds__(BG_THREADS) void gemm_big_kernel(GemmArgs a, int n_
 
 bool gemm_tiled_supported(int epi, const GemmArgs &a) {
   if (a.M < 1 || a.N < 16 || a.N % 16 || a.K < 8 || a.K % 8 || a.ldx % 8 || a.row_bnd != nullptr) return false;
+  if (a.part != nullptr && a.row_rsc == nullptr) return false;   // the row scales come precomputed
   if ((a.M + TB_ROWS - 1) / TB_ROWS > 65535) return false;
   switch (epi) {
     case EPI_PLAIN: return a.ld_out % 4 == 0;
@@ -371,6 +440,13 @@ bool gemm_tiled_supported(int epi, const GemmArgs &a) {
     case EPI_SWIGLU: return a.ld_act % 4 == 0;
     default: return false;
   }
+}
+
+hipError_t launch_row_scale(const float *part, int n_part, int M, float inv_d, float eps, float *out, hipStream_t s) {
+  if (part == nullptr || out == nullptr || n_part < 1 || M < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(row_scale_kernel, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, part, n_part, M, inv_d, eps,
+                     out);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s) {
