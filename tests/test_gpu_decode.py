@@ -361,12 +361,14 @@ def test_large_prompt_batch_prefill_matches_batch_one():
     assert t2 == t1
 
 
-@pytest.mark.parametrize("P", [1, 45, 97, 300, 3100])
-def test_gqa128_prefill_ragged_prompts(P):
+@pytest.mark.parametrize("P,G", [(1, 4), (45, 4), (97, 4), (300, 4), (3100, 4), (97, 1), (300, 2), (45, 8),
+                                 (300, 8)])
+def test_gqa128_prefill_ragged_prompts(P, G):
     """The 32-layer model's attention shape (head_dim 128, four query heads
-    per kv head) on a 2-layer model small enough for the float64 oracle, with
-    prompt lengths that are not multiples of the 32-query / 64-key blocks of
-    the prompt attention (and the one-token prompt), at batch 2: y_0 and the
+    per kv head; also one, two and eight) on a 2-layer model small enough for
+    the float64 oracle, with prompt lengths that are not multiples of the
+    32-query / 64-key blocks of the prompt attention (and the one-token
+    prompt), at batch 2: y_0 and the
     next tokens follow the oracle (near ties aside) and every decoded row's
     exit logits agree within 2e-2 (max relative).  At 2 x 3100 prompt rows
     all four prompt GEMMs (QKV with RoPE and the cache write, O and down with
@@ -376,7 +378,7 @@ def test_gqa128_prefill_ragged_prompts(P):
     from paper_2606_29223_amd import dexlib
     cfg = configs.scaled_down(configs.get("llama-32L-d4096-x8-w4"), n_layers=2, d_model=1024, d_ffn=2048,
                               vocab=4096)
-    cfg.update(n_heads=8, n_kv_heads=2, head_dim=128, prompt_len=P, batch=2, prompt_seeds=[7201, 7202])
+    cfg.update(n_heads=2 * G, n_kv_heads=2, head_dim=128, prompt_len=P, batch=2, prompt_seeds=[7201, 7202])
     w = gen.generate_model(cfg)
     T = 5
     dec = dexlib.Decoder(cfg, dexlib.device_weights(cfg, w), explored=[cfg["n_layers"]], width_cap=1,
