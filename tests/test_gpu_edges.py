@@ -7,6 +7,10 @@
     position, every sequence stops with exactly max_context - prompt_len
     generated tokens (sequences of one batch reach it in different rounds),
     the tokens equal plain AR's, and further steps report DEX_E_CAPACITY;
+  * a round at the row capacity: 32 sequences of width 8 make up to
+    DEX_MAX_ROWS = 256 rows a round (stage GEMMs over several 64-row
+    blocks, the exit head over every row, many attention groups), and the
+    tokens are still plain AR's;
   * the degenerate lattice of width 1: only the anchor advances, so every
     commit takes exactly N rounds from a fresh anchor, and the tokens are
     still AR's (Algorithm 1 with no parallel branch is sequential
@@ -19,7 +23,7 @@ import pytest
 import oracle
 from oracle import dex
 from synth import configs, gen
-from tests.gpu_common import decoder, host_weights, torch_cuda
+from tests.gpu_common import decoder, host_weights, run, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -96,6 +100,25 @@ def test_decoding_stops_exactly_at_max_context(X, W):
     assert toks == ar_toks
     assert ar_rounds == T - 1                     # AR commits once per round
     assert rounds > ar_rounds
+
+
+@pytest.mark.parametrize("name,X", [(TINY, [1, 2, 3, 4]), ("small-12L-d768-bf16", [3, 6, 9, 12])])
+def test_rows_per_round_at_the_maximum(name, X):
+    torch_cuda()
+    cfg = configs.get(name)
+    B, W, T = 32, 8, 10
+    assert B * W == 256                           # DEX_MAX_ROWS
+    P = cfg["prompt_len"]
+    prompts = np.stack([gen.tokens(gen.mix64(900 + s), P, cfg["vocab"]) for s in range(B)])
+    dec = decoder(name, explored=X, width_cap=W, batch=B, max_context=P + 4 * T)
+    toks, rounds = run(dec, prompts, T)
+    dec.close()
+    most = max(len(r["rows"]) for r in rounds)
+    assert most == B * W                          # a round at the capacity
+    ar_dec = decoder(name, explored=[cfg["n_layers"]], width_cap=1, batch=B, max_context=P + 4 * T)
+    ar_toks, _ = run(ar_dec, prompts, T)
+    ar_dec.close()
+    assert np.array_equal(toks, ar_toks)
 
 
 def test_width_one_commits_every_n_rounds():
