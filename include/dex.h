@@ -25,10 +25,16 @@
  *   - Every call returns dex_status; DEX_OK is 0, errors are negative.  No
  *     C++ exception crosses the ABI.  dex_last_error(ctx) gives a message
  *     (dex_last_error(NULL): the last dex_create failure of this thread).
- *   - Weights are borrowed DEVICE memory: the caller keeps them alive and
- *     unchanged until dex_destroy.  Every array is row-major; a projection
- *     matrix is [out_features][in_features].  The library owns the key/value
- *     caches, the lattice state and all scratch memory.
+ *   - Weights are passed as DEVICE memory, row-major; a projection matrix is
+ *     [out_features][in_features].  dex_create repacks every projection
+ *     matrix and the LM head into the library's own streaming layout, so a
+ *     context holds a second, library-owned copy of those weights (one more
+ *     model's worth of device memory: about 14.2 GB for a 32-layer d_model
+ *     4096 model) until dex_destroy.  The caller's embedding table and norm
+ *     gains stay borrowed: keep them alive and unchanged until dex_destroy
+ *     (the caller's projection and LM-head arrays may be freed once
+ *     dex_create has returned).  The library also owns the key/value caches,
+ *     the lattice state and all scratch memory.
  *   - Host arrays passed in or out are caller-owned and only accessed during
  *     the call.
  *   - All device work is enqueued on config.hip_stream (NULL = the default
@@ -91,8 +97,9 @@ enum {
  * head h / (n_heads / n_kv_heads).  `weight_dtype` is the element type of the
  * embedding, the projections and the LM head, and also of the key/value
  * cache and the activations fed to the matrix cores; norm gains are float.
- * Requirements: d_model, head_dim multiples of 16; head_dim <= 128;
- * n_heads a multiple of n_kv_heads; n_heads/n_kv_heads <= 8.             */
+ * Requirements: d_model a multiple of 16; head_dim 32, 64 or 128; n_heads
+ * a multiple of n_kv_heads; n_heads/n_kv_heads <= 8 (DEX_E_INVAL from
+ * dex_create otherwise).                                                   */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rope_theta, rms_eps, residual_scale;
@@ -178,6 +185,29 @@ const char *dex_last_error(const dex_ctx *ctx);
 /* ---------------------------------------------------------------------------
  * Inspection taps for tests and the benchmark.
  * ------------------------------------------------------------------------- */
+
+/* The work items the planner picks for one lattice state (host only: no
+ * context and no GPU are needed).  Algorithm 1's expansion with the
+ * eligibility of the one-explorer-per-device pipeline (a non-anchor slot
+ * advances only when every ancestor has completed more stages) and the
+ * width-cap priority (not in the paper, which names branch pruning as future
+ * work): the anchor's advance first, then the width_cap - 1 other items of
+ * lowest (hypothesis cost, path length, path), where a path is the string of
+ * depth steps (a slot's stage k to k+1) and position steps (a slot's stage f
+ * to the stage-0 node of the slot forked there) from the anchor's stage-0
+ * node to the item's node, compared with the depth step first, and the
+ * hypothesis cost is the sum of f + 1 over the fork stages f on it.
+ *   slots      host [n_slots][4 + n_explored] int32, canonical order, slot 0
+ *              the anchor: parent (-1 for slot 0, else an earlier slot),
+ *              fork stage (< the parent's c, <= n_explored - 2; at most one
+ *              child per (parent, stage)), c (completed stages), absolute
+ *              position, then the candidates u[0..c-1] (the rest ignored)
+ *   out        host [capacity][3] int32: kind (0 advance, 1 fork), slot,
+ *              fork stage (-1 for advance), in priority order; *n_out = count
+ * width_cap 0 = uncapped.  Malformed slots or too small a capacity:
+ * DEX_E_INVAL (*n_out still receives the count in the latter case).        */
+dex_status dex_debug_plan(int32_t n_explored, int32_t width_cap, int32_t decs, int32_t max_context,
+                          const int32_t *slots, int32_t n_slots, int32_t *out, int32_t capacity, int32_t *n_out);
 
 /* While enabled, every dex_step writes the float32 exit logits (before the
  * DECS mask) of each round row r to device_buf + r * vocab.  capacity_rows

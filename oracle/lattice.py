@@ -26,12 +26,22 @@ One round:
     binary expansion (2^q - 1 nodes after q rounds).
   * width cap W (not in the paper, which names branch pruning as future
     work): keep the anchor item and the W-1 others of lowest
-    (hypothesis cost, path length, path) where a path is the list of fork
-    stages leading from the anchor to the item and its hypothesis cost is
-    sum(f + 1) over it.  Parity unpinned: the paper fixes no pruning rule,
-    so a capped trace is pinned only by invariants (losslessness, at most W
-    rows a round, eligibility) and, for W >= 2^(N-1), by the paper's
-    uncapped lattice, which the rule must reproduce exactly.
+    (hypothesis cost, path length, path).  The lattice is the binary tree of
+    Section 3.2 rooted at the anchor's stage-0 node: a depth step D goes from
+    a slot's stage-k node to its stage-(k+1) node, a position step P from a
+    slot's stage-f node to the stage-0 node of the slot forked there.  An
+    item's path is the step string from the root to the node it evaluates
+    (advance(s): s's stage c_s node; fork(s, f): the new slot's stage-0
+    node), its length the number of steps, and paths of equal length compare
+    lexicographically with D before P.  Path length then lexicographic order
+    is the paper's node numbering (depth child 2i+1, position child 2i+2)
+    read relative to the current anchor.  The hypothesis cost is
+    sum(f + 1) over the fork stages f on the path (each P step costs one
+    plus the D steps taken in its slot before it), i.e. the length of the
+    path up to its last P step.  The paper fixes no pruning rule; the order
+    is pinned by hand-derived lattice states (tests/golden/
+    width_cap_order.json) and, for W >= 2^(N-1), by the paper's uncapped
+    lattice, which the rule must reproduce exactly.
   * DECS (greedy): a node's candidate is the argmax with the tokens already
     proposed by shallower nodes of the same slot masked out, except the
     anchor's final-depth node, which is never masked.  decs=False masks
@@ -89,7 +99,21 @@ class Slot:
 
 
 def hypothesis_cost(path) -> int:
+    """sum(f + 1) over the fork stages f of a path (the width-cap priority)."""
     return sum(f + 1 for f in path)
+
+
+DEPTH_STEP, POSITION_STEP = 0, 1     # lexicographic order: depth step first
+
+
+def steps_of_forks(forks) -> tuple:
+    """Step string from the anchor's stage-0 node to the stage-0 node of the
+    slot reached by forking at stages `forks` (anchor first): each fork at
+    stage f is f depth steps inside its slot, then one position step."""
+    out = []
+    for f in forks:
+        out += [DEPTH_STEP] * f + [POSITION_STEP]
+    return tuple(out)
 
 
 @dataclass
@@ -160,17 +184,30 @@ class Lattice:
         return items
 
     @staticmethod
-    def item_path(item):
+    def item_forks(item):
+        """Fork stages from the anchor down to the item's slot (a fork item's
+        own fork last)."""
         kind, s, f = item
         return s.path() + ((f,) if kind == "fork" else ())
+
+    @staticmethod
+    def item_steps(item):
+        """Step string from the anchor's stage-0 node to the item's node."""
+        kind, s, f = item
+        if kind == "fork":
+            return steps_of_forks(s.path() + (f,))
+        return steps_of_forks(s.path()) + (DEPTH_STEP,) * s.c
+
+    def priority(self, item):
+        steps = self.item_steps(item)
+        return (hypothesis_cost(self.item_forks(item)), len(steps), steps)
 
     def select(self):
         items = self.eligible()
         first = items[0]
         assert first[0] == "advance" and first[1] is self.anchor
         rest = items[1:]
-        rest.sort(key=lambda it: (hypothesis_cost(self.item_path(it)), len(self.item_path(it)),
-                                  self.item_path(it)))
+        rest.sort(key=self.priority)
         if self.width_cap > 0:
             rest = rest[: self.width_cap - 1]
         return [first] + rest

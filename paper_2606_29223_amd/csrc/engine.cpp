@@ -50,10 +50,16 @@ struct Seq {
   int last_fresh = -1, last_committed_pos = -1;
 };
 
+// Width-cap priority of a work item.  The lattice is a binary tree rooted at
+// the anchor's stage-0 node: a depth step (0) goes from a slot's stage k to
+// stage k+1, a position step (1) from a slot's stage f to the stage-0 node of
+// the slot forked there.  `steps` leads from the root to the node the item
+// evaluates; `cost` is the hypothesis cost, sum(f + 1) over the fork stages
+// on the way (the length of the path up to its last position step).
 struct Item {
   int kind;                 // 0 advance, 1 fork
   int slot, f;
-  std::vector<int> path;
+  std::vector<unsigned char> steps;
   int cost;
 };
 
@@ -63,11 +69,19 @@ struct Timing {
   double bytes;
 };
 
+// (hypothesis cost, path length, path with the depth step first): path
+// length then lexicographic order is the paper's node numbering (depth child
+// 2i+1, position child 2i+2) relative to the current anchor.
 inline bool item_less(const Item &a, const Item &b) {
   if (a.cost != b.cost) return a.cost < b.cost;
-  if (a.path.size() != b.path.size()) return a.path.size() < b.path.size();
-  return a.path < b.path;
+  if (a.steps.size() != b.steps.size()) return a.steps.size() < b.steps.size();
+  return a.steps < b.steps;
 }
+
+// What the planner needs to know of a context.
+struct PlanRule {
+  int N, W, decs, max_ctx;
+};
 
 }  // namespace
 
@@ -245,38 +259,47 @@ std::vector<int> ancestors(const Seq &s, int i) {   // anchor first, parent last
 // completed more stages at round start; fork every completed stage f <= N-2
 // not yet forked (without DECS, not when its token repeats a shallower fork
 // of the same slot); width cap keeps the anchor and the W-1 items of lowest
-// (hypothesis cost, path length, path).
-std::vector<Item> plan_items(const dex_ctx *ctx, const Seq &s) {
+// (hypothesis cost, path length, path) -- item_less.
+std::vector<Item> plan_items(const PlanRule &rule, const Seq &s) {
   std::vector<Item> items;
-  const int N = ctx->N;
+  const int N = rule.N;
   for (int i = 0; i < (int)s.slots.size(); ++i) {
     const Slot &sl = s.slots[i];
-    const std::vector<int> path = slot_path(s, i);
+    std::vector<unsigned char> root;          // steps to this slot's stage-0 node
     int cost = 0;
-    for (int f : path) cost += f + 1;
+    for (int f : slot_path(s, i)) {
+      root.insert(root.end(), (size_t)f, (unsigned char)0);
+      root.push_back(1);
+      cost += f + 1;
+    }
     bool adv = (i == 0);
     if (!adv) {
       adv = true;
       for (int a : ancestors(s, i))
         if (s.slots[a].c <= sl.c) { adv = false; break; }
     }
-    if (adv) items.push_back({0, i, -1, path, cost});
-    if (sl.pos + 1 > ctx->max_ctx - 1) continue;
+    if (adv) {
+      std::vector<unsigned char> st = root;
+      st.insert(st.end(), (size_t)sl.c, (unsigned char)0);
+      items.push_back({0, i, -1, st, cost});
+    }
+    if (sl.pos + 1 > rule.max_ctx - 1) continue;
     for (int f = 0; f < std::min(sl.c, N - 1); ++f) {
       if (sl.child[f] >= 0) continue;
-      if (!ctx->decs) {
+      if (!rule.decs) {
         bool dup = false;
         for (int g = 0; g < f; ++g) dup |= (sl.u[g] == sl.u[f]);
         if (dup) continue;
       }
-      std::vector<int> p2 = path;
-      p2.push_back(f);
-      items.push_back({1, i, f, p2, cost + f + 1});
+      std::vector<unsigned char> st = root;
+      st.insert(st.end(), (size_t)f, (unsigned char)0);
+      st.push_back(1);
+      items.push_back({1, i, f, st, cost + f + 1});
     }
   }
   std::vector<Item> rest(items.begin() + 1, items.end());
   std::sort(rest.begin(), rest.end(), item_less);
-  if (ctx->W > 0 && (int)rest.size() > ctx->W - 1) rest.resize(ctx->W - 1);
+  if (rule.W > 0 && (int)rest.size() > rule.W - 1) rest.resize(rule.W - 1);
   std::vector<Item> out;
   out.push_back(items[0]);
   out.insert(out.end(), rest.begin(), rest.end());
@@ -528,6 +551,8 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       m->d_ffn < 1 || m->vocab < 2)
     return bad("model dimensions out of range");
   if (m->n_heads / m->n_kv_heads > 8) return bad("n_heads / n_kv_heads must be <= 8");
+  // the attention kernels exist for these head sizes only
+  if (m->head_dim != 32 && m->head_dim != 64 && m->head_dim != 128) return bad("head_dim must be 32, 64 or 128");
   if (m->weight_dtype != DEX_F32 && m->weight_dtype != DEX_BF16) return bad("weight_dtype must be DEX_F32 or DEX_BF16");
   const int epb = m->weight_dtype == DEX_BF16 ? 8 : 4;
   if (m->d_ffn % epb || (m->n_heads * m->head_dim) % epb) return bad("d_ffn must be a multiple of 8 (bf16) / 4 (f32)");
@@ -944,7 +969,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     Seq &s = ctx->seqs[si];
     if (!s.active) continue;
     q_start[si] = s.slots[0].c;
-    std::vector<Item> items = plan_items(ctx, s);
+    std::vector<Item> items = plan_items(PlanRule{ctx->N, ctx->W, ctx->decs, ctx->max_ctx}, s);
     for (const Item &it : items) {
       if (it.kind == 0) {
         rows.push_back({si, it.slot, s.slots[it.slot].c});
@@ -1205,6 +1230,42 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     c.slots2 = 2 * ctx->S; c.d = ctx->d; c.n_part = ctx->n_part; c.N = N; c.max_ctx = ctx->max_ctx; c.S = ctx->S;
     TimedLaunch tl(ctx, 7, 0.0);
     HIPCHK(launch_collapse(c, ctx->stream));
+  }
+  return DEX_OK;
+}
+
+dex_status dex_debug_plan(int32_t n_explored, int32_t width_cap, int32_t decs, int32_t max_context,
+                          const int32_t *slots, int32_t n_slots, int32_t *out, int32_t capacity, int32_t *n_out) {
+  const int N = n_explored;
+  if (N < 1 || N > DEX_MAX_EXPLORED || width_cap < 0 || max_context < 2 || !slots || n_slots < 1 || !out ||
+      !n_out || capacity < 0)
+    return DEX_E_INVAL;
+  const int st = 4 + N;
+  Seq s;
+  s.slots.resize(n_slots);
+  for (int i = 0; i < n_slots; ++i) {
+    const int32_t *r = slots + (size_t)i * st;
+    Slot &sl = s.slots[i];
+    sl.parent = r[0]; sl.fork_stage = r[1]; sl.c = r[2]; sl.pos = r[3];
+    if ((i == 0) != (sl.parent < 0) || sl.parent >= i || sl.c < 0 || sl.c > N) return DEX_E_INVAL;
+    if (i > 0 && (sl.fork_stage < 0 || sl.fork_stage >= s.slots[sl.parent].c || sl.fork_stage > N - 2))
+      return DEX_E_INVAL;
+    sl.u.assign(r + 4, r + 4 + sl.c);
+    sl.child.assign(N, -1);
+    if (i > 0) {
+      Slot &p = s.slots[sl.parent];
+      if (p.child[sl.fork_stage] >= 0) return DEX_E_INVAL;
+      p.child[sl.fork_stage] = i;
+      sl.x = p.u[sl.fork_stage];
+    }
+  }
+  const std::vector<Item> items = plan_items(PlanRule{N, width_cap, decs ? 1 : 0, max_context}, s);
+  *n_out = (int)items.size();
+  if ((int)items.size() > capacity) return DEX_E_INVAL;
+  for (size_t j = 0; j < items.size(); ++j) {
+    out[3 * j] = items[j].kind;
+    out[3 * j + 1] = items[j].slot;
+    out[3 * j + 2] = items[j].f;
   }
   return DEX_OK;
 }

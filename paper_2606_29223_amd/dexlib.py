@@ -26,7 +26,7 @@ EXPORTED = (
     "dex_debug_set_logits_tap", "dex_debug_lattice", "dex_debug_last_collapse",
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
     "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_attention",
-    "dex_debug_gumbel", "dex_debug_copy",
+    "dex_debug_gumbel", "dex_debug_copy", "dex_debug_plan",
 )
 
 
@@ -104,6 +104,7 @@ def load(path: str | None = None):
     lib.dex_debug_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, i32, P(i32), P(i32), P(i32),
                                         P(i32), P(i32), i32, vp, vp]
     lib.dex_debug_gumbel.argtypes = [ctypes.c_uint64, i32, i32, i32, vp, vp]
+    lib.dex_debug_plan.argtypes = [i32, i32, i32, i32, P(i32), i32, P(i32), i32, P(i32)]
     for name in EXPORTED:
         if name not in ("dex_destroy", "dex_last_error"):
             getattr(lib, name).restype = ctypes.c_int32
@@ -154,6 +155,23 @@ def dex_step(ctx, batch: int, info: DexStepInfo | None = None) -> np.ndarray:
 
 def dex_destroy(ctx) -> None:
     load().dex_destroy(ctx)
+
+
+def dex_debug_plan(n_explored: int, width_cap: int, decs: int, max_context: int, slots) -> list:
+    """Planner tap (host only): slots = [(parent, fork_stage, c, pos, u), ...]
+    in canonical order; returns [(kind, slot, f)] in priority order."""
+    lib = load()
+    n = len(slots)
+    rec = np.full((n, 4 + n_explored), -1, dtype=np.int32)
+    for i, (par, f, c, pos, u) in enumerate(slots):
+        rec[i, :4] = (par, f, c, pos)
+        rec[i, 4:4 + len(u)] = u
+    cap = 4 * n * n_explored + 1
+    out = np.empty((cap, 3), dtype=np.int32)
+    cnt = ctypes.c_int32()
+    _check(lib, None, lib.dex_debug_plan(n_explored, width_cap, decs, max_context, _i32p(rec), n, _i32p(out), cap,
+                                         ctypes.byref(cnt)))
+    return [tuple(int(v) for v in out[j]) for j in range(cnt.value)]
 
 
 # ---------------------------------------------------------------- convenience

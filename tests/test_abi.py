@@ -71,7 +71,8 @@ def test_create_rejects_bad_explored_sets(lib, X, W, B, msg):
 
 
 def test_create_rejects_bad_dims(lib):
-    for kw in (dict(d_model=100), dict(head_dim=24), dict(n_kv_heads=3), dict(weight_dtype=7)):
+    for kw in (dict(d_model=100), dict(head_dim=24), dict(n_kv_heads=3), dict(weight_dtype=7),
+               dict(head_dim=16), dict(head_dim=48), dict(head_dim=80), dict(head_dim=96), dict(head_dim=112)):
         m, _a, _f = _model(**kw)
         c, _x = _config([4])
         ctx = ctypes.c_void_p()
