@@ -287,6 +287,30 @@ dex_status dex_debug_attention(int32_t dtype, int32_t head_dim, int32_t n_heads,
                                const int32_t *row_nc, const int32_t *chain_off, const int32_t *chain,
                                int32_t chain_len, void *out, void *hip_stream);
 
+/* dex_debug_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): same arguments, same kernels and the same output bits, but
+ * the row tables and split partials live in a fixed array of 64 MiB that
+ * the library holds on every GPU it runs on until the process ends (the
+ * first call on a device resolves that device's copy; the call runs on the
+ * current device, which must own hip_stream).  No hipMalloc, hipFree or
+ * other allocating routine is called.  Limits: n_rows <= DEX_MAX_ROWS,
+ * chain_len <= 16384, and n_rows * n_heads * (max row_pos / 64 + 1) *
+ * (head_dim + 2) * 4 bytes of split partials <= 63.75 MiB (at head_dim 128
+ * and 32 heads: 8 rows up to 32128 keys each); beyond them
+ * the call returns DEX_E_CAPACITY before any device work, with the reason
+ * in dex_last_error(NULL).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other threads, other streams) race and must
+ * be serialised by the caller.  Nothing in the array needs to start at zero
+ * (every partial the combine reads is written by the same call).
+ * Synchronises hip_stream.                                                  */
+dex_status dex_debug_attention_noalloc(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                       int32_t batch, int32_t kv_entries, const void *k_cache,
+                                       const void *v_cache, const float *q, int32_t n_rows,
+                                       const int32_t *row_seq, const int32_t *row_pos, const int32_t *row_nc,
+                                       const int32_t *chain_off, const int32_t *chain, int32_t chain_len,
+                                       void *out, void *hip_stream);
+
 /* The Gumbel source of sampling mode (Algorithm 2 draws one Gumbel row per
  * sampling slot; here the row of a slot is a function of (seed, sequence,
  * position of the slot's input token), so plain autoregressive sampling at

@@ -20,6 +20,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -509,6 +510,138 @@ dex_status fail_mid_round(dex_ctx *ctx, const char *msg, dex_status s) {
   ctx->err = msg;
   ctx->poisoned = true;
   return s;
+}
+
+// ------------------------------------------------ stand-alone attention
+// One call of the stand-alone decode attention (the arguments of
+// dex_debug_attention).
+struct AttnCall {
+  int dtype, head_dim, n_heads, n_kv_heads, batch, kv_entries;
+  const void *k_cache, *v_cache;
+  const float *q;
+  int n_rows;
+  const int32_t *row_seq, *row_pos, *row_nc, *chain_off, *chain;
+  int chain_len;
+  void *out;
+};
+
+// Offsets (in ints) of the device row tables, the row-group count, the split
+// count and the split partials' size of one call.
+struct AttnTab {
+  size_t o_pos, o_nc, o_seq, o_coff, o_g0, o_gn, o_gs, o_chain, n_ints;
+  int ng, n_splits;
+  size_t part_bytes;
+};
+
+size_t attention_table_ints(int n_rows, int chain_len) { return 7 * (size_t)n_rows + (size_t)chain_len + 1; }
+
+// Validates a call on the host (nothing is launched for a bad one) and
+// writes its row tables to tab (cap ints, at least attention_table_ints):
+// row groups are consecutive rows of one sequence sharing their committed
+// prefix, at most 64 (row, query head) pairs' worth of rows each.
+dex_status attention_tables(const AttnCall &c, int *tab, size_t cap, AttnTab *t) {
+  if (c.dtype != DEX_F32 && c.dtype != DEX_BF16) return DEX_E_INVAL;
+  if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 128) return DEX_E_INVAL;
+  if (c.n_kv_heads < 1 || c.n_heads < c.n_kv_heads || c.n_heads % c.n_kv_heads || c.n_heads / c.n_kv_heads > 8)
+    return DEX_E_INVAL;
+  if (c.batch < 1 || c.kv_entries < 1 || c.n_rows < 1 || c.chain_len < 0) return DEX_E_INVAL;
+  if (!c.k_cache || !c.v_cache || !c.q || !c.out || !c.row_seq || !c.row_pos || !c.row_nc || !c.chain_off)
+    return DEX_E_INVAL;
+  if (c.chain_len > 0 && !c.chain) return DEX_E_INVAL;
+  if (cap < attention_table_ints(c.n_rows, c.chain_len)) return DEX_E_INVAL;
+  int maxpos = 0;
+  for (int r = 0; r < c.n_rows; ++r) {
+    const int sq = c.row_seq[r], pos = c.row_pos[r], nc = c.row_nc[r], co = c.chain_off[r];
+    if (sq < 0 || sq >= c.batch || pos < 0 || pos >= c.kv_entries || nc < 0 || nc > pos + 1) return DEX_E_INVAL;
+    if (pos - nc >= ATT_SPLIT) return DEX_E_INVAL;
+    if (nc <= pos && (co < 0 || (int64_t)co + (pos - nc) >= c.chain_len)) return DEX_E_INVAL;
+    for (int i = 0; nc + i <= pos; ++i)
+      if (c.chain[co + i] < 0 || c.chain[co + i] >= c.kv_entries) return DEX_E_INVAL;
+    maxpos = std::max(maxpos, pos);
+  }
+  t->n_splits = maxpos / ATT_SPLIT + 1;
+  if (t->n_splits > ATT_MAX_SPLITS) return DEX_E_INVAL;
+  const int R = c.n_rows;
+  t->o_pos = 0; t->o_nc = R; t->o_seq = 2 * (size_t)R; t->o_coff = 3 * (size_t)R; t->o_g0 = 4 * (size_t)R;
+  std::copy(c.row_pos, c.row_pos + R, tab + t->o_pos);
+  std::copy(c.row_nc, c.row_nc + R, tab + t->o_nc);
+  std::copy(c.row_seq, c.row_seq + R, tab + t->o_seq);
+  std::copy(c.chain_off, c.chain_off + R, tab + t->o_coff);
+  const int G = c.n_heads / c.n_kv_heads, grp_rows = std::max(1, ATT_MAX_PAIRS / G);
+  int ng = 0;
+  int *g0 = tab + t->o_g0;
+  for (int r = 0; r < R;) {                 // group starts; sizes and sequences below
+    int e = r;
+    while (e < R && c.row_seq[e] == c.row_seq[r] && c.row_nc[e] == c.row_nc[r] && e - r < grp_rows) ++e;
+    g0[ng++] = r;
+    r = e;
+  }
+  t->ng = ng;
+  t->o_gn = t->o_g0 + ng; t->o_gs = t->o_gn + ng; t->o_chain = t->o_gs + ng;
+  for (int g = 0; g < ng; ++g) {
+    const int e = g + 1 < ng ? g0[g + 1] : R;
+    tab[t->o_gn + g] = e - g0[g];
+    tab[t->o_gs + g] = c.row_seq[g0[g]];
+  }
+  if (c.chain_len > 0) std::copy(c.chain, c.chain + c.chain_len, tab + t->o_chain);
+  else tab[t->o_chain] = 0;
+  t->n_ints = t->o_chain + std::max(c.chain_len, 1);
+  t->part_bytes = (size_t)R * c.n_heads * t->n_splits * (c.head_dim + 2) * 4;
+  return DEX_OK;
+}
+
+// The decode attention and its split combine over device tables dtab (laid
+// out by attention_tables) with split partials in part.
+hipError_t launch_attention_call(const AttnCall &c, const AttnTab &t, const int *dtab, float *part,
+                                 hipStream_t st) {
+  AttnArgs a{};
+  a.q = c.q; a.ldq = c.n_heads * c.head_dim; a.kc = c.k_cache; a.vc = c.v_cache; a.kv_entries = c.kv_entries;
+  a.n_kv_heads = c.n_kv_heads; a.n_heads = c.n_heads; a.head_dim = c.head_dim; a.batch = c.batch;
+  a.grp_row0 = dtab + t.o_g0; a.grp_nrows = dtab + t.o_gn; a.grp_seq = dtab + t.o_gs;
+  a.row_pos = dtab + t.o_pos; a.row_nc = dtab + t.o_nc; a.row_chain_off = dtab + t.o_coff;
+  a.chain = dtab + t.o_chain; a.row_seq = dtab + t.o_seq; a.n_rows = c.n_rows; a.part = part;
+  a.jmax = t.n_splits; a.n_splits = t.n_splits; a.scale = 1.0f / std::sqrt((float)c.head_dim);
+  hipError_t e = launch_attention(c.dtype, a, t.ng, st);
+  CombineArgs cb{};
+  cb.part = part; cb.row_pos = dtab + t.o_pos; cb.jmax = t.n_splits; cb.n_heads = c.n_heads;
+  cb.head_dim = c.head_dim; cb.out = c.out; cb.ld_out = c.n_heads * c.head_dim;
+  if (e == hipSuccess) e = launch_combine(c.dtype, cb, c.n_rows, st);
+  return e;
+}
+
+// ------------------------------------------ fixed scratch (no allocation)
+// dex_debug_attention_noalloc keeps its row tables and split partials in
+// this array instead of allocating them.  Host code never uses the array's
+// name as a device address: scratch_address() resolves it once per device
+// (with that device current) and every kernel argument, copy or fill uses
+// the resolved address.
+constexpr size_t kScratchBytes = 64ull << 20;
+constexpr size_t kScratchTableBytes = 256ull << 10;
+constexpr int kNoallocMaxChain = 16384;
+constexpr size_t kNoallocTableInts = 7 * DEX_MAX_ROWS + kNoallocMaxChain + 1;
+static_assert(kNoallocTableInts * 4 <= kScratchTableBytes, "row tables fit their scratch region");
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_addr[kMaxDevices] = {};
+
+hipError_t scratch_address(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace
@@ -1423,65 +1556,63 @@ dex_status dex_debug_attention(int32_t dtype, int32_t head_dim, int32_t n_heads,
                                const float *q, int32_t n_rows, const int32_t *row_seq, const int32_t *row_pos,
                                const int32_t *row_nc, const int32_t *chain_off, const int32_t *chain,
                                int32_t chain_len, void *out, void *stream) {
-  if (dtype != DEX_F32 && dtype != DEX_BF16) return DEX_E_INVAL;
-  if (head_dim != 32 && head_dim != 64 && head_dim != 128) return DEX_E_INVAL;
-  if (n_kv_heads < 1 || n_heads < n_kv_heads || n_heads % n_kv_heads || n_heads / n_kv_heads > 8) return DEX_E_INVAL;
-  if (batch < 1 || kv_entries < 1 || n_rows < 1 || chain_len < 0) return DEX_E_INVAL;
-  if (!k_cache || !v_cache || !q || !out || !row_seq || !row_pos || !row_nc || !chain_off) return DEX_E_INVAL;
-  if (chain_len > 0 && !chain) return DEX_E_INVAL;
-  int maxpos = 0;
-  for (int r = 0; r < n_rows; ++r) {
-    const int sq = row_seq[r], pos = row_pos[r], nc = row_nc[r], co = chain_off[r];
-    if (sq < 0 || sq >= batch || pos < 0 || pos >= kv_entries || nc < 0 || nc > pos + 1) return DEX_E_INVAL;
-    if (pos - nc >= ATT_SPLIT) return DEX_E_INVAL;
-    if (nc <= pos && (co < 0 || (int64_t)co + (pos - nc) >= chain_len)) return DEX_E_INVAL;
-    for (int t = 0; nc + t <= pos; ++t)
-      if (chain[co + t] < 0 || chain[co + t] >= kv_entries) return DEX_E_INVAL;
-    maxpos = std::max(maxpos, pos);
-  }
-  const int n_splits = maxpos / ATT_SPLIT + 1;
-  if (n_splits > ATT_MAX_SPLITS) return DEX_E_INVAL;
-  // row groups: consecutive rows of one sequence sharing their committed
-  // prefix, at most 64 (row, query head) pairs' worth of rows each
-  const int G = n_heads / n_kv_heads, grp_rows = std::max(1, ATT_MAX_PAIRS / G);
-  std::vector<int> g0, gn, gs;
-  for (int r = 0; r < n_rows;) {
-    int e = r;
-    while (e < n_rows && row_seq[e] == row_seq[r] && row_nc[e] == row_nc[r] && e - r < grp_rows) ++e;
-    g0.push_back(r); gn.push_back(e - r); gs.push_back(row_seq[r]);
-    r = e;
-  }
-  const int ng = (int)g0.size();
-  std::vector<int> tab;
-  auto put = [&](const int32_t *p, int n) { const size_t o = tab.size(); tab.insert(tab.end(), p, p + n); return o; };
-  const size_t o_pos = put(row_pos, n_rows), o_nc = put(row_nc, n_rows), o_seq = put(row_seq, n_rows);
-  const size_t o_coff = put(chain_off, n_rows), o_g0 = put(g0.data(), ng), o_gn = put(gn.data(), ng);
-  const size_t o_gs = put(gs.data(), ng), o_chain = tab.size();
-  if (chain_len > 0) tab.insert(tab.end(), chain, chain + chain_len);
-  else tab.push_back(0);
+  const AttnCall c{dtype, head_dim, n_heads, n_kv_heads, batch, kv_entries, k_cache, v_cache, q, n_rows,
+                   row_seq, row_pos, row_nc, chain_off, chain, chain_len, out};
+  if (n_rows < 1 || chain_len < 0) return DEX_E_INVAL;
+  std::vector<int> tab(attention_table_ints(n_rows, chain_len));
+  AttnTab t{};
+  const dex_status vs = attention_tables(c, tab.data(), tab.size(), &t);
+  if (vs != DEX_OK) return vs;
   const hipStream_t st = (hipStream_t)stream;
-  const size_t part_bytes = (size_t)n_rows * n_heads * n_splits * (head_dim + 2) * 4;
   int *dtab = nullptr;
   float *part = nullptr;
-  if (hipMalloc((void **)&dtab, tab.size() * 4) != hipSuccess) return DEX_E_NOMEM;
-  if (hipMalloc((void **)&part, part_bytes) != hipSuccess) { (void)hipFree(dtab); return DEX_E_NOMEM; }
-  hipError_t e = hipMemcpyAsync(dtab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice, st);
-  AttnArgs a{};
-  a.q = q; a.ldq = n_heads * head_dim; a.kc = k_cache; a.vc = v_cache; a.kv_entries = kv_entries;
-  a.n_kv_heads = n_kv_heads; a.n_heads = n_heads; a.head_dim = head_dim; a.batch = batch;
-  a.grp_row0 = dtab + o_g0; a.grp_nrows = dtab + o_gn; a.grp_seq = dtab + o_gs;
-  a.row_pos = dtab + o_pos; a.row_nc = dtab + o_nc; a.row_chain_off = dtab + o_coff; a.chain = dtab + o_chain;
-  a.row_seq = dtab + o_seq; a.n_rows = n_rows; a.part = part; a.jmax = n_splits; a.n_splits = n_splits;
-  a.scale = 1.0f / std::sqrt((float)head_dim);
-  if (e == hipSuccess) e = launch_attention(dtype, a, ng, st);
-  CombineArgs c{};
-  c.part = part; c.row_pos = dtab + o_pos; c.jmax = n_splits; c.n_heads = n_heads; c.head_dim = head_dim;
-  c.out = out; c.ld_out = n_heads * head_dim;
-  if (e == hipSuccess) e = launch_combine(dtype, c, n_rows, st);
+  if (hipMalloc((void **)&dtab, t.n_ints * 4) != hipSuccess) return DEX_E_NOMEM;
+  if (hipMalloc((void **)&part, t.part_bytes) != hipSuccess) { (void)hipFree(dtab); return DEX_E_NOMEM; }
+  hipError_t e = hipMemcpyAsync(dtab, tab.data(), t.n_ints * 4, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = launch_attention_call(c, t, dtab, part, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   else (void)hipStreamSynchronize(st);
   (void)hipFree(part);
   (void)hipFree(dtab);
+  return e == hipSuccess ? DEX_OK : DEX_E_HIP;
+}
+
+dex_status dex_debug_attention_noalloc(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                       int32_t batch, int32_t kv_entries, const void *k_cache,
+                                       const void *v_cache, const float *q, int32_t n_rows,
+                                       const int32_t *row_seq, const int32_t *row_pos, const int32_t *row_nc,
+                                       const int32_t *chain_off, const int32_t *chain, int32_t chain_len,
+                                       void *out, void *stream) {
+  g_create_error.clear();
+  const AttnCall c{dtype, head_dim, n_heads, n_kv_heads, batch, kv_entries, k_cache, v_cache, q, n_rows,
+                   row_seq, row_pos, row_nc, chain_off, chain, chain_len, out};
+  if (n_rows < 1 || chain_len < 0) return DEX_E_INVAL;
+  if (n_rows > DEX_MAX_ROWS || chain_len > kNoallocMaxChain) {
+    g_create_error = "dex_debug_attention_noalloc: more than 256 rows or 16384 chain entries";
+    return DEX_E_CAPACITY;
+  }
+  // host staging of the tables: a fixed per-thread array (no allocation)
+  thread_local int tab[kNoallocTableInts];
+  AttnTab t{};
+  const dex_status vs = attention_tables(c, tab, kNoallocTableInts, &t);
+  if (vs != DEX_OK) return vs;
+  if (t.part_bytes > kScratchBytes - kScratchTableBytes) {
+    g_create_error = "dex_debug_attention_noalloc: split partials exceed the 63.75 MiB scratch";
+    return DEX_E_CAPACITY;
+  }
+  void *base = nullptr;
+  hipError_t e = scratch_address(&base);
+  if (e != hipSuccess) {
+    g_create_error = std::string("scratch address: ") + hipGetErrorString(e);
+    return DEX_E_HIP;
+  }
+  const hipStream_t st = (hipStream_t)stream;
+  int *dtab = (int *)base;
+  float *part = (float *)((char *)base + kScratchTableBytes);
+  e = hipMemcpyAsync(dtab, tab, t.n_ints * 4, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = launch_attention_call(c, t, dtab, part, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  else (void)hipStreamSynchronize(st);
   return e == hipSuccess ? DEX_OK : DEX_E_HIP;
 }
 

@@ -26,7 +26,7 @@ EXPORTED = (
     "dex_debug_set_logits_tap", "dex_debug_lattice", "dex_debug_last_collapse",
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
     "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_attention",
-    "dex_debug_gumbel", "dex_debug_copy", "dex_debug_plan",
+    "dex_debug_gumbel", "dex_debug_copy", "dex_debug_plan", "dex_debug_attention_noalloc",
 )
 
 
@@ -103,6 +103,7 @@ def load(path: str | None = None):
     lib.dex_debug_copy.argtypes = [vp, vp, i64, vp]
     lib.dex_debug_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, i32, P(i32), P(i32), P(i32),
                                         P(i32), P(i32), i32, vp, vp]
+    lib.dex_debug_attention_noalloc.argtypes = list(lib.dex_debug_attention.argtypes)
     lib.dex_debug_gumbel.argtypes = [ctypes.c_uint64, i32, i32, i32, vp, vp]
     lib.dex_debug_plan.argtypes = [i32, i32, i32, i32, P(i32), i32, P(i32), i32, P(i32)]
     for name in EXPORTED:

@@ -115,3 +115,25 @@ def test_debug_attention_rejects_bad_tables(lib):
     for kw in bad:
         assert call(**kw) == dexlib.DEX_E_INVAL, kw
 
+
+
+def test_attention_noalloc_rejects_before_any_device_call(lib):
+    """The no-allocation attention refuses bad tables (DEX_E_INVAL) and sizes
+    beyond its fixed scratch (DEX_E_CAPACITY) on the host."""
+    fake = 0x1000
+    arr = lambda v: (ctypes.c_int32 * len(v))(*v)
+
+    def call(n_rows=1, pos=10, nc=10, chain=(50,), E=100, H=32, Hkv=8, hd=128):
+        seq = [0] * n_rows
+        return lib.dex_debug_attention_noalloc(1, hd, H, Hkv, 1, E, fake, fake, fake, n_rows, arr(seq),
+                                               arr([pos] * n_rows), arr([nc] * n_rows), arr([0] * n_rows),
+                                               arr(chain), len(chain), fake, None)
+
+    assert call(nc=12) == dexlib.DEX_E_INVAL
+    assert call(hd=48) == dexlib.DEX_E_INVAL
+    assert call(n_rows=257, E=300) == dexlib.DEX_E_CAPACITY
+    assert "256 rows" in lib.dex_last_error(None).decode()
+    assert call(chain=tuple([50] * 16385), E=20000) == dexlib.DEX_E_CAPACITY
+    # 8 rows x 32 heads x 516 splits x 130 floats x 4 B = 68.7 MB of partials (> 63.75 MiB)
+    assert call(n_rows=8, pos=33000, nc=33000, chain=(33010,), E=33100) == dexlib.DEX_E_CAPACITY
+    assert "scratch" in lib.dex_last_error(None).decode()
