@@ -82,3 +82,50 @@ def check_tokens_teacher_forced(z_oracle_final: np.ndarray, gpu_tokens) -> list:
 
 def max_rel_err(z_gpu: np.ndarray, z_ref: np.ndarray) -> float:
     return float(np.max(np.abs(z_gpu - z_ref)) / np.max(np.abs(z_ref)))
+
+
+class NodeOracle:
+    """Exit logits of any lattice node, recomputed by the float64 oracle from
+    the node's own token prefix (Section 3.2, lattice expansion: a node at
+    position p with input token x decodes the prefix committed tokens ||
+    inputs of its ancestor slots || x, at the depth of its stage).
+
+    A prefix is keyed by its tokens at positions P .. p (P = prompt length);
+    each key's per-layer hidden states and keys/values are computed once, up
+    to the deepest layer asked for, against the prompt's keys/values and
+    the states of the key's own shorter prefixes."""
+
+    def __init__(self, model, prompt_len: int, prefill):
+        self.m = model
+        self.P = prompt_len
+        self.Kp, self.Vp, _ = prefill
+        self.memo = {}
+
+    def _states(self, key: tuple, depth: int) -> dict:
+        st = self.memo.setdefault(key, {"h": [], "k": [], "v": []})
+        done = len(st["h"])
+        if done >= depth:
+            return st
+        prev = [self._states(key[:i], depth) for i in range(1, len(key))]
+        pos = self.P + len(key) - 1
+        h = self.m.embed(key[-1]) if done == 0 else st["h"][-1]
+        for l in range(done, depth):
+            pk = np.concatenate([self.Kp[l][: self.P]] + [p["k"][l][None] for p in prev], axis=0)
+            pv = np.concatenate([self.Vp[l][: self.P]] + [p["v"][l][None] for p in prev], axis=0)
+            h, k, v = self.m.layer_row(l, h, pos, pk, pv)
+            st["h"].append(h)
+            st["k"].append(k)
+            st["v"].append(v)
+        return st
+
+    def logits(self, key, depth: int) -> np.ndarray:
+        return self.m.exit_logits(self._states(tuple(int(t) for t in key), depth)["h"][depth - 1])
+
+
+def node_key(generated, lat_slot, prompt_len: int) -> tuple:
+    """Token key of an oracle-lattice slot: the committed generated tokens
+    before the anchor's position, then the inputs of the slot chain from the
+    anchor down to the slot."""
+    chain = lat_slot.ancestors() + [lat_slot]
+    anchor_pos = chain[0].pos
+    return tuple(int(t) for t in generated[: anchor_pos - prompt_len]) + tuple(int(s.x) for s in chain)

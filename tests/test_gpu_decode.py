@@ -18,8 +18,8 @@ import oracle
 from oracle import ar, dex
 from oracle.lattice import Lattice
 from synth import configs, gen
-from tests.gpu_common import (GAP, LOGIT_RTOL, check_tokens_teacher_forced, decoder, device_weights, host_weights,
-                              max_rel_err, torch_cuda)
+from tests.gpu_common import (GAP, LOGIT_RTOL, NodeOracle, check_tokens_teacher_forced, decoder, device_weights,
+                              host_weights, max_rel_err, node_key, torch_cuda)
 
 pytestmark = pytest.mark.gpu
 
@@ -53,9 +53,11 @@ def _run(dec, prompts, T, tap=None, collapse=True):
     return np.array(toks), rounds
 
 
-def _replay(rounds, N, W, decs, max_ctx, y0, P, seq=0):
+def _replay(rounds, N, W, decs, max_ctx, y0, P, seq=0, on_row=None):
     """Feed the GPU's candidate tokens to the oracle lattice; every planning
-    and collapse decision must agree."""
+    and collapse decision must agree.  on_row(round, gpu_row_index,
+    oracle_row) is called for each of the sequence's rows before the round's
+    candidates are inserted (the oracle row's slot chain is then the node's)."""
     lat = Lattice(N, W, bool(decs), max_ctx, int(y0), P)
     for i, rd in enumerate(rounds):
         if not any(r[0] == seq for r in rd["rows"]):
@@ -65,6 +67,10 @@ def _replay(rounds, N, W, decs, max_ctx, y0, P, seq=0):
         order = sorted(range(len(orc)), key=lambda j: orc[j][1])
         gpu = [(r[1], r[2], r[3], r[4]) for r in rd["rows"] if r[0] == seq]
         assert [orc[j] for j in order] == [g[:3] for g in gpu], f"round {i}"
+        if on_row is not None:
+            gidx = [r for r, row in enumerate(rd["rows"]) if row[0] == seq]
+            for k, j in enumerate(order):
+                on_row(i, gidx[k], rows[j])
         toks = [0] * len(rows)
         for k, j in enumerate(order):
             toks[j] = gpu[k][3]
@@ -245,6 +251,42 @@ def test_small_bf16_lossless_and_oracle():
             if slot == 0:
                 worst = max(worst, max_rel_err(rd["logits"][r], z[pos - P, stage]))
     assert worst <= LOGIT_RTOL, worst
+
+
+def test_small_bf16_every_row_logits():
+    """Every row of every round -- speculative nodes included, whose
+    attention reads their ancestor slots' keys/values -- against the float64
+    oracle recomputing that node from its own prefix (committed tokens, then
+    the inputs of its slot chain) at its stage's depth: max relative error of
+    the exit logits (before the DECS mask) within 2e-2 (12-layer bf16 model,
+    explored depths {3,6,9,12}, width 4, 48 tokens)."""
+    torch = torch_cuda()
+    cfg, w = host_weights(SMALL)
+    P, T = cfg["prompt_len"], 48
+    prompt = gen.prompts(cfg)
+    dec = decoder(SMALL, max_context=P + T)
+    tap = torch.empty((cfg["width_cap"], cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    toks, rounds = _run(dec, prompt, T, tap=tap)
+    dec.close()
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    pl = [int(t) for t in prompt[0]]
+    no = NodeOracle(m, P, m.prefill(pl))
+    seq = [int(t) for t in toks[0]]
+    X = cfg["explored"]
+    stats = {"worst": 0.0, "rows": 0, "speculative": 0}
+
+    def on_row(i, r, orow):
+        key = node_key(seq, orow.slot, P)
+        z = no.logits(key, X[orow.stage])
+        stats["worst"] = max(stats["worst"], max_rel_err(rounds[i]["logits"][r], z))
+        stats["rows"] += 1
+        stats["speculative"] += orow.slot.parent is not None
+
+    _replay(rounds, len(X), cfg["width_cap"], cfg["decs"], P + T, seq[0], P, on_row=on_row)
+    assert stats["rows"] == sum(len(rd["rows"]) for rd in rounds)
+    assert stats["speculative"] >= 40, stats
+    assert stats["worst"] <= LOGIT_RTOL, stats
 
 
 @pytest.mark.parametrize("X,W,decs", [([2, 4, 6, 8, 10, 12], 8, 1), ([6, 12], 2, 1), ([3, 6, 9, 12], 4, 0),

@@ -1,14 +1,17 @@
 """GPU: the 32-layer d4096 GQA workloads at full size, in the configuration
 the benchmark times (prompt length, explored depths, width caps).
 
-The batch-8 workload with 8192-token prompts is too large for the float64
-oracle's prefill; it is checked through the properties alone.
 Properties that hold at any size are checked exhaustively: DEX committed
 tokens equal the same library's plain AR tokens bit for bit, the lattice
 trace equals the oracle lattice driven by the GPU's candidates, and the
 key/value collapse gather is bit-exact.  The float64 oracle re-scores a few
 sampled positions of the GPU's sequence one by one (teacher-forced tokens and
-per-depth exit logits).
+per-depth exit logits) and, on the batch-1 workload, every row of the first
+rounds, speculative nodes included.  The batch-8 workload with 8192-token
+prompts is too large for the float64 oracle's prefill at full depth and
+width; its decode shape (GQA head_dim 128, 8 lattices of 8192-token prompts,
+width 8, up to 64 rows a round) is compared with the oracle row by row on a
+4-layer, d_model-1024 model instead.
 """
 import numpy as np
 import pytest
@@ -16,7 +19,8 @@ import pytest
 import oracle
 from oracle import ar
 from synth import configs, gen
-from tests.gpu_common import LOGIT_RTOL, check_tokens_teacher_forced, max_rel_err, torch_cuda
+from tests.gpu_common import (GAP, LOGIT_RTOL, NodeOracle, check_tokens_teacher_forced, max_rel_err, node_key,
+                              torch_cuda)
 from tests.test_gpu_decode import _replay, _run, _snapshot
 
 pytestmark = pytest.mark.gpu
@@ -140,3 +144,96 @@ def test_oracle_sampled_positions_full_size(llama, name):
                 seen += 1
     assert seen >= n_pos
     assert worst <= LOGIT_RTOL, worst
+    if name != C3:
+        return
+    # every row of the first six rounds, speculative nodes included: the
+    # oracle recomputes each node from its own prefix at its stage's depth
+    no = NodeOracle(m, P, pf)
+    X = cfg["explored"]
+    stats = {"worst": 0.0, "rows": 0, "speculative": 0}
+
+    def on_row(i, r, orow):
+        if i >= 6:
+            return
+        z = no.logits(node_key(seq, orow.slot, P), X[orow.stage])
+        stats["worst"] = max(stats["worst"], max_rel_err(rounds[i]["logits"][r], z))
+        stats["rows"] += 1
+        stats["speculative"] += orow.slot.parent is not None
+
+    _replay(rounds, len(X), cfg["width_cap"], cfg["decs"], P + T, seq[0], P, on_row=on_row)
+    assert stats["rows"] == sum(len(rd["rows"]) for rd in rounds[:6])
+    assert stats["speculative"] >= 6, stats
+    assert stats["worst"] <= LOGIT_RTOL, stats
+
+
+def _c5_shape():
+    """The long-context batched workload's decode shape on a model small
+    enough for the float64 oracle: 4 layers, d_model 1024, 8 query heads over
+    2 kv heads of head_dim 128 (the 32-layer model's GQA group of 4), every
+    layer explored, width 8, 8 sequences with 8192-token prompts."""
+    cfg = configs.scaled_down(configs.get(C5), n_layers=4, d_model=1024, d_ffn=3584)
+    cfg.update(n_heads=8, n_kv_heads=2, head_dim=128)
+    assert cfg["explored"] == [1, 2, 3, 4] and cfg["width_cap"] == 8 and cfg["batch"] == 8
+    assert cfg["prompt_len"] == 8192
+    return cfg
+
+
+@pytest.mark.timeout(600)
+def test_c5_shape_reduced_depth_matches_oracle():
+    """8 lattices of 8192-token prompts decoded as one batch (up to 64 rows a
+    round, 129 key splits per row): DEX tokens equal plain AR bit for bit for
+    every sequence, every sequence's trace equals the oracle lattice's, and
+    for sequences 0 and 7 the float64 oracle re-scores every row of every
+    round from the node's own prefix -- committed tokens follow the oracle
+    (top-2 gap rule, teacher-forced) and every row's exit logits agree
+    within 2e-2."""
+    import concurrent.futures as cf
+
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = _c5_shape()
+    w = gen.generate_model(cfg)
+    dev = dexlib.device_weights(cfg, w)
+    P, T, B = cfg["prompt_len"], 10, cfg["batch"]
+    prompt = gen.prompts(cfg)
+    ar_dec = _decoder(cfg, dev, explored=[cfg["n_layers"]], width_cap=1, max_context=P + T)
+    ar_toks, _ = _run(ar_dec, prompt, T, collapse=False)
+    ar_dec.close()
+    dec = _decoder(cfg, dev, max_context=P + T)
+    tap = torch.empty((B * cfg["width_cap"], cfg["vocab"]), dtype=torch.float32, device="cuda")
+    dec.set_logits_tap(tap)
+    toks, rounds = _run(dec, prompt, T, tap=tap)
+    dec.close()
+    del dev, tap
+    torch.cuda.empty_cache()
+    assert np.array_equal(toks, ar_toks)
+    assert max(len(rd["rows"]) for rd in rounds) > 32          # rounds of more than 32 rows occurred
+    X = cfg["explored"]
+    m = oracle.Model(cfg, gen.model_as_f64(cfg, w))
+    checked = (0, 7)
+    with cf.ThreadPoolExecutor(len(checked)) as ex:
+        prefills = list(ex.map(lambda b: m.prefill([int(t) for t in prompt[b]]), checked))
+    for b, pf in zip(checked, prefills):
+        no = NodeOracle(m, P, pf)
+        seq = [int(t) for t in toks[b]]
+        z0 = m.exit_logits(pf[2])
+        zf = np.stack([z0] + [no.logits(seq[:t], cfg["n_layers"]) for t in range(1, T)])
+        check_tokens_teacher_forced(zf[1:], seq)                 # y_1 .. y_{T-1}
+        if seq[0] != int(np.argmax(z0)):                         # y_0: the prompt's last position
+            srt = np.sort(z0)
+            assert srt[-1] - srt[-2] < GAP and z0.max() - z0[seq[0]] < GAP
+        stats = {"worst": 0.0, "rows": 0, "speculative": 0}
+
+        def on_row(i, r, orow, no=no, seq=seq, stats=stats):
+            z = no.logits(node_key(seq, orow.slot, P), X[orow.stage])
+            stats["worst"] = max(stats["worst"], max_rel_err(rounds[i]["logits"][r], z))
+            stats["rows"] += 1
+            stats["speculative"] += orow.slot.parent is not None
+
+        _replay(rounds, len(X), cfg["width_cap"], cfg["decs"], P + T, seq[0], P, seq=b, on_row=on_row)
+        assert stats["rows"] == sum(1 for rd in rounds for r in rd["rows"] if r[0] == b)
+        assert stats["speculative"] >= 10, (b, stats)
+        assert stats["worst"] <= LOGIT_RTOL, (b, stats)
+    for b in range(B):
+        if b not in checked:
+            _replay(rounds, len(X), cfg["width_cap"], cfg["decs"], P + T, toks[b][0], P, seq=b)
