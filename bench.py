@@ -17,12 +17,15 @@ Prints one JSON line.  Besides the contract fields it carries
                attention's key/value reads) and the resulting HBM-roofline
                tokens/s of this schedule;
   e2e          committed tokens/s including the prefill (y_0 counts);
-  step_traffic HBM bytes per round counted by rocprofv3 (FETCH_SIZE +
-               WRITE_SIZE over the same rounds, profiles/step_traffic.json,
-               only while the kernel sources are unchanged) over this run's
-               time per round;
+  step_traffic HBM bytes per round of this run's own rounds: its algorithmic
+               bytes (weights of the stages each round ran, the exit head,
+               the attention's key/value reads) times the counted/algorithmic
+               ratio that rocprofv3 measured over whole decode rounds of the
+               same workload (FETCH_SIZE + WRITE_SIZE, profiles/
+               step_traffic.json, only while the kernel and engine sources
+               are unchanged), over this run's time per round;
   cpu_baseline the oracle (float64 numpy) running the same decode on the host
-               cores for a bounded sample.
+               cores for a bounded sample, DEX and plain AR timed separately.
 """
 
 from __future__ import annotations
@@ -59,14 +62,16 @@ def parse():
                    help="attach synthetic inducing adapters with this gate to the non-final depths")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     p.add_argument("--step-traffic-json", default=os.path.join(ROOT, "profiles", "step_traffic.json"))
+    p.add_argument("--kernel-stats-json", default=os.path.join(ROOT, "profiles", "kernel_stats.json"))
     return p.parse_args()
 
 
 def cpu_baseline(cfg, weights, prompts, budget_s, temperature=0.0, seed=0):
-    """The oracle as it stands, timed on this host: DEX rounds on the first
-    sequence after its prefill (prefill untimed)."""
+    """The oracle as it stands, timed on this host after its prefill of
+    sequence 0 (prefill untimed): DEX rounds (the value), then plain greedy
+    AR over a budget of a third of DEX's."""
     import oracle
-    from oracle import dex
+    from oracle import ar, dex
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -75,24 +80,32 @@ def cpu_baseline(cfg, weights, prompts, budget_s, temperature=0.0, seed=0):
     m = oracle.Model(cfg, gen.model_as_f64(cfg, weights))
     prompt = [int(t) for t in prompts[0]]
     pf = m.prefill(prompt)
-    # run DEX for growing T until the budget is used; report the last full run
-    T, t_used, commits, rounds = 2, 0.0, 0, 0
-    while True:
-        t0 = time.perf_counter()
-        r = dex.dex_generate(m, prompt, cfg["explored"], cfg["width_cap"], bool(cfg["decs"]), T,
-                             prefill=pf, keep_trace=False, temperature=temperature, seed=seed)
-        dt = time.perf_counter() - t0
-        t_used, commits, rounds = dt, T - 1, r.rounds
-        if dt * 2.5 > budget_s or T >= cfg["gen_len"]:
-            break
-        T = min(cfg["gen_len"], T * 2)
+
+    def grow(run, budget):
+        # run for growing T until the budget is used; report the last full run
+        T = 2
+        while True:
+            t0 = time.perf_counter()
+            extra = run(T)
+            dt = time.perf_counter() - t0
+            if dt * 2.5 > budget or T >= cfg["gen_len"]:
+                return T - 1, dt, extra
+            T = min(cfg["gen_len"], T * 2)
+
+    commits, t_used, rounds = grow(
+        lambda T: dex.dex_generate(m, prompt, cfg["explored"], cfg["width_cap"], bool(cfg["decs"]), T,
+                                   prefill=pf, keep_trace=False, temperature=temperature, seed=seed).rounds,
+        budget_s)
+    ar_commits, ar_used, _ = grow(
+        lambda T: ar.ar_generate(m, prompt, T, prefill=pf, temperature=temperature, seed=seed), budget_s / 3)
     cores = len(os.sched_getaffinity(0))
     return {
         "value": commits / t_used, "unit": "committed tokens/s", "cores": blas_threads or cores,
         "kind": "oracle",
-        "sample": f"float64 oracle DEX on sequence 0 of {cfg['name']}: {cfg['prompt_len']}-token prompt "
-                  f"(prefill untimed), {commits} commits in {rounds} rounds, {t_used:.1f} s; "
-                  f"host affinity {cores} cores",
+        "ar_value": ar_commits / ar_used,
+        "sample": f"float64 oracle on sequence 0 of {cfg['name']} after its {cfg['prompt_len']}-token prompt "
+                  f"(prefill untimed): DEX {commits} commits in {rounds} rounds, {t_used:.1f} s; plain AR "
+                  f"{ar_commits} tokens in {ar_used:.1f} s (ar_value); host affinity {cores} cores",
     }
 
 
@@ -138,6 +151,8 @@ def main():
 
     ad_runs = [0]       # non-final stages with exit rows: each streams its adapter
 
+    attn_total = [0.0]  # algorithmic bytes of the attention launches
+
     def steps(n):
         commits = rounds = layers = row_layers = 0
         for _ in range(n):
@@ -146,6 +161,7 @@ def main():
             rounds += 1
             layers += dec.info.layers_streamed
             row_layers += dec.info.row_layers
+            attn_total[0] += dec.info.attn_bytes
             ns = sum(1 for k in range(dec.N) if dec.info.rows_per_stage[k])
             stages_hist[ns] = stages_hist.get(ns, 0) + 1
             for k in range(dec.N):
@@ -168,6 +184,7 @@ def main():
     kstar_hist.clear()
     stages_hist.clear()
     ad_runs[0] = 0
+    attn_total[0] = 0.0
     t0 = time.perf_counter()
     commits, rounds, layers, row_layers = steps(args.steps)
     torch.cuda.synchronize()
@@ -180,6 +197,22 @@ def main():
     stages_timed = dict(stages_hist)
     m_timed = dict(m_hist)
     ad_runs_timed = ad_runs[0]
+    attn_bytes_per_round = attn_total[0] / max(rounds, 1)   # K/V, q and outputs of the attention
+
+    # a pass of the same length with events at the round boundaries only
+    # (the schedule of the timed steps): where a round's wall time goes,
+    # including the gap between rounds
+    dec.set_round_timing(True)
+    tr0 = time.perf_counter()
+    steps(args.steps)
+    torch.cuda.synchronize()
+    tr_wall = (time.perf_counter() - tr0) / args.steps * 1e3
+    rt_ms, rt_n = dec.round_times()
+    dec.set_round_timing(False)
+    round_phases = {"wall_ms_per_round": round(tr_wall, 4), "rounds": rt_n}
+    for i, nm in enumerate(dexlib.ROUND_PHASES):
+        cnt = rt_n - 1 if nm in ("commit_collapse", "gap_before_round") else rt_n
+        round_phases[nm + "_ms"] = round(rt_ms[i] / max(cnt, 1), 4)
 
     # instrumented run of the same length: per-kernel HIP event durations
     # (each launch bracketed by events; includes the event overhead)
@@ -188,7 +221,6 @@ def main():
     torch.cuda.synchronize()
     ms, n, nbytes = dec.kernel_times()
     dec.set_timing(False)
-    attn_bytes_per_round = nbytes[1] / max(args.steps, 1)   # K/V, q and outputs of the attention
     names = dexlib.KERNEL_CLASSES
     per_kernel = {names[i]: {"ms": round(ms[i], 3), "launches": int(n[i]),
                              "avg_us_event": round(ms[i] / max(n[i], 1) * 1e3, 2),
@@ -216,21 +248,56 @@ def main():
             traffic = None
     roofline = {"bound": "hbm", "kernel": names[dom], "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "frac_source": "mean of 96 back-to-back launches of the class at the most common rows per "
+                               "stage (HIP events on the decode stream, layers cycled)",
                 "bytes_per_launch": bytes_per, "avg_launch_us": round(avg_us, 2), "rows": m_mode}
+    # the same class inside the steps: events around each launch of the
+    # instrumented rerun (all stages on one stream), and, when a kernel trace
+    # of this benchmark's own command exists for the current sources, the
+    # rocprofv3 average duration of the class
+    if n[dom]:
+        ev_us = ms[dom] / n[dom] * 1e3
+        ev_bytes = nbytes[dom] / n[dom]
+        roofline["in_step_events"] = {"avg_launch_us": round(ev_us, 2),
+                                      "frac": round(ev_bytes / (ev_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    if os.path.exists(args.kernel_stats_json):
+        from paper_2606_29223_amd.profile_summary import csrc_source_hash
+        try:
+            ks = json.load(open(args.kernel_stats_json))
+            ent = ks.get("classes", {}).get(names[dom])
+            if ent and ks.get("source") == csrc_source_hash() and ks.get("config") == cfg["name"]:
+                roofline["rocprof"] = {"avg_launch_us": round(ent["avg_us"], 2), "launches": ent["launches"],
+                                       "frac": round(bytes_per / (ent["avg_us"] * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                                       "profile": os.path.relpath(args.kernel_stats_json, ROOT)}
+        except (OSError, ValueError, KeyError):
+            pass
 
-    # whole-round traffic counted for the same rounds with the current sources
+    # whole-round traffic: this run's algorithmic bytes per round times the
+    # counted/algorithmic ratio measured over whole rounds with the current
+    # sources
     step_traffic = None
-    if os.path.exists(args.step_traffic_json) and args.temperature == 0.0 and args.adapter_alpha is None:
+    L, N = cfg["n_layers"], len(cfg["explored"])
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    d, F, V = cfg["d_model"], cfg["d_ffn"], cfg["vocab"]
+    layer_bytes = es * (d * (cfg["n_heads"] + 2 * cfg["n_kv_heads"]) * cfg["head_dim"]
+                        + cfg["n_heads"] * cfg["head_dim"] * d + 3 * d * F)
+    ad_bytes = (ad_runs_timed * 2 * d * (2 * d) * es) if args.adapter_alpha is not None else 0
+    alg_per_round = (layers * layer_bytes + rounds * es * V * d + ad_bytes) / max(rounds, 1) + attn_bytes_per_round
+    if os.path.exists(args.step_traffic_json) and args.adapter_alpha is None:
         from paper_2606_29223_amd.profile_summary import csrc_source_hash
         try:
             st = json.load(open(args.step_traffic_json))
-            if (st.get("source") == csrc_source_hash() and st.get("config") == cfg["name"]
-                    and st.get("warmup") == args.warmup and st.get("rounds") == args.steps):
-                gbs = st["counted_bytes_per_round"] / (elapsed / args.steps) / 1e9
-                step_traffic = {"counted_bytes_per_round": st["counted_bytes_per_round"],
-                                "algorithmic_bytes_per_round": st["algorithmic_bytes_per_round"],
+            if st.get("source") == csrc_source_hash() and st.get("config") == cfg["name"]:
+                ratio = st["counted_bytes_per_round"] / st["algorithmic_bytes_per_round"]
+                counted = ratio * alg_per_round
+                gbs = counted / (elapsed / args.steps) / 1e9
+                step_traffic = {"counted_over_algorithmic": round(ratio, 5),
+                                "ratio_measured_over": f"rounds {st['warmup'] + 1}..{st['warmup'] + st['rounds']} "
+                                                       f"of {st['config']} ({os.path.relpath(args.step_traffic_json, ROOT)})",
+                                "algorithmic_bytes_per_round": alg_per_round,
+                                "counted_bytes_per_round": counted,
                                 "achieved_GBps": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
-        except (OSError, ValueError, KeyError):
+        except (OSError, ValueError, KeyError, ZeroDivisionError):
             step_traffic = None
 
     ar_value = None
@@ -248,12 +315,6 @@ def main():
         ar_value = na / (time.perf_counter() - ta)
         ar.close()
 
-    L, N = cfg["n_layers"], len(cfg["explored"])
-    es = 2 if cfg["dtype"] == "bf16" else 4
-    d, F, V = cfg["d_model"], cfg["d_ffn"], cfg["vocab"]
-    layer_bytes = es * (d * (cfg["n_heads"] + 2 * cfg["n_kv_heads"]) * cfg["head_dim"]
-                        + cfg["n_heads"] * cfg["head_dim"] * d + 3 * d * F)
-    ad_bytes = (ad_runs_timed * 2 * d * (2 * d) * es) if args.adapter_alpha is not None else 0
     bytes_per_commit = (layers * layer_bytes + rounds * es * V * d + ad_bytes) / max(commits, 1)
     hbm_bytes_per_commit = bytes_per_commit + attn_bytes_per_round * rounds / max(commits, 1)
     cpu = None
@@ -297,6 +358,7 @@ def main():
                 "roofline_tokens_per_s": round(PEAK_HBM_GBS * 1e9 / hbm_bytes_per_commit, 2),
                 "frac_of_schedule_roofline": round(value * hbm_bytes_per_commit / (PEAK_HBM_GBS * 1e9), 4),
                 "achieved_GBps": round(value * hbm_bytes_per_commit / 1e9, 1)},
+        "round_phases": round_phases,
         "prefill_s": round(prefill_s, 3),
         "e2e_tokens_per_s": round(e2e, 3),
         "ar_tokens_per_s": round(ar_value, 3) if ar_value else None,

@@ -157,6 +157,10 @@ typedef struct {
   int32_t row_pos[DEX_MAX_ROWS];        /* absolute position of the row's input token */
   int32_t row_token[DEX_MAX_ROWS];      /* decoded candidate (DECS argmax) of the row */
   int64_t rounds_total;                 /* dex_step calls so far */
+  double attn_bytes;                    /* algorithmic bytes of the round's attention: keys and
+                                           values of every position up to each row group's
+                                           deepest row, at every layer it ran, plus the
+                                           queries read and the outputs written */
 } dex_step_info;
 
 /* Validate the model and X, derive the stages, allocate caches and scratch.
@@ -241,6 +245,21 @@ dex_status dex_debug_slot_entry(dex_ctx *ctx, int32_t seq, int32_t slot, int32_t
  * launches (weights + activations + keys/values they read or write).          */
 dex_status dex_debug_set_kernel_timing(dex_ctx *ctx, int32_t enable);
 dex_status dex_debug_kernel_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *launches, double *bytes);
+
+/* Round phases: while enabled, dex_step records events on the decode stream
+ * at its boundaries.  dex_debug_round_times fills, summed over the rounds
+ * since the last enable (*rounds of them), in milliseconds:
+ *   ms[0] row-table upload           ms[1] stage sweep (all lanes joined)
+ *   ms[2] exit head, verify/commit    ms[3] result copy to the host
+ *   ms[4] host commit handling and the collapse gather (from the copy's
+ *         end to the collapse's end; one round fewer than *rounds)
+ *   ms[5] the gap before a round: from the previous round's last device
+ *         work to this round's upload (return to the caller, the caller's
+ *         own work, the next call's planning; one round fewer)
+ *   ms[6] host planning (dex_step entry to the upload, host clock)
+ * n <= 7 entries are written.                                               */
+dex_status dex_debug_set_round_timing(dex_ctx *ctx, int32_t enable);
+dex_status dex_debug_round_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *rounds);
 
 /* Mean duration of one decode-step GEMM class (3 o-proj, 4 gate/up, 5 down,
  * 6 lm-head) at M rows: `reps` back-to-back launches on the context's stream

@@ -17,6 +17,7 @@
 // the decoded candidates and commits per round.
 #include <algorithm>
 #include <array>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -33,6 +34,9 @@ namespace {
 
 // streams a round's stages are spread over unless the caller says otherwise
 constexpr int kDefaultStageStreams = 4;
+
+// round phases reported by dex_debug_round_times
+constexpr int kRoundPhases = 7;
 
 thread_local std::string g_create_error;
 
@@ -150,6 +154,14 @@ struct dex_ctx {
   std::vector<Timing> pending;
   double t_ms[8] = {0}, t_bytes[8] = {0};
   int64_t t_n[8] = {0};
+  // round phases: events on the decode stream at the round's boundaries
+  // (two sets, the previous round's last event opens the gap before this one)
+  bool round_timing = false;
+  hipEvent_t rt_ev[2][6] = {};
+  int rt_cur = 0;
+  bool rt_prev = false;
+  double rt_ms[kRoundPhases] = {0};
+  int64_t rt_rounds = 0;
   std::vector<void *> allocs;
 };
 
@@ -669,6 +681,8 @@ void dex_destroy(dex_ctx *ctx) {
     (void)hipStreamDestroy(ctx->lane_st[i]);
   }
   for (auto e : ctx->lane_ev) if (e) (void)hipEventDestroy(e);
+  for (auto &set : ctx->rt_ev)
+    for (auto e : set) if (e) (void)hipEventDestroy(e);
   if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
   delete ctx;
 }
@@ -1090,6 +1104,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   if (!ctx->prefilled) { ctx->err = "dex_step before dex_prefill"; return DEX_E_STATE; }
   if (!committed_out) { ctx->err = "committed is NULL"; return DEX_E_INVAL; }
   const int N = ctx->N, B = ctx->B;
+  const auto t_call = std::chrono::steady_clock::now();
   for (int s = 0; s < B; ++s) committed_out[s] = -1;
   bool any = false;
   for (auto &s : ctx->seqs) any |= s.active;
@@ -1195,7 +1210,13 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   }
   const size_t tab_ints = (size_t)(t_rcommit - T) + R;
   if (tab_ints > ctx->tab_cap) return fail_mid_round(ctx, "row table overflow", DEX_E_CAPACITY);
+  hipEvent_t *rt = ctx->round_timing ? ctx->rt_ev[ctx->rt_cur] : nullptr;
+  if (rt) {
+    ctx->rt_ms[6] += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_call).count();
+    HIPCHK(hipEventRecord(rt[0], ctx->stream));
+  }
   HIPCHK(hipMemcpyAsync(ctx->tab_dev, T, tab_ints * 4, hipMemcpyHostToDevice, ctx->stream));
+  if (rt) HIPCHK(hipEventRecord(rt[1], ctx->stream));
   const int *D = ctx->tab_dev;
   auto dptr = [&](const int *hp) { return D + (hp - T); };
 
@@ -1212,6 +1233,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     for (int i = 1; i < ctx->n_lanes; ++i) HIPCHK(hipStreamWaitEvent(ctx->lane_st[i], ctx->fork_ev, 0));
   }
   int layers_streamed = 0, row_layers = 0, lane_next = 0;
+  double attn_bytes = 0.0;
   for (int k = 0; k < N; ++k) {
     const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
     if (M == 0) continue;
@@ -1234,6 +1256,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     }
     t.n_splits = std::min(ctx->jmax, stage_maxpos / ATT_SPLIT + 1);
     t.attn_bytes += (double)M * ctx->H * ctx->hd * (4.0 + ctx->es);
+    attn_bytes += t.attn_bytes * (double)ls.size();
     {
       PrepArgs p{};
       p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
@@ -1261,13 +1284,33 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     }
   }
   // ---------------------------------------------------- exit + commit
+  if (rt) HIPCHK(hipEventRecord(rt[2], ctx->stream));
   dex_status xs = run_exit(ctx, R, dptr(t_bnd), ctx->bnd_h, ctx->bnd_part, dptr(t_maskn), dptr(t_mask),
                            dptr(t_cidx), ctx->cand, dptr(t_seq), dptr(t_pos), stage_r0.data(), dptr(t_rcommit));
   if (xs != DEX_OK) return fail(ctx, xs);
+  if (rt) HIPCHK(hipEventRecord(rt[3], ctx->stream));
   // candidates, then (token, k*) of the committing sequences, in one copy
   HIPCHK(hipMemcpyAsync(ctx->res_host, ctx->u_dev, (R + 2 * commit_seqs.size()) * 4, hipMemcpyDeviceToHost,
                         ctx->stream));
+  if (rt) HIPCHK(hipEventRecord(rt[4], ctx->stream));
   HIPCHK(hipStreamSynchronize(ctx->stream));
+  if (rt) {
+    // this round's device phases; the previous round's collapse (its host
+    // commit handling and the gather) and the gap before this round
+    float ms = 0.f;
+    for (int i = 0; i < 4; ++i) {
+      HIPCHK(hipEventElapsedTime(&ms, rt[i], rt[i + 1]));
+      ctx->rt_ms[i] += ms;
+    }
+    if (ctx->rt_prev) {
+      hipEvent_t *pv = ctx->rt_ev[1 - ctx->rt_cur];
+      HIPCHK(hipEventElapsedTime(&ms, pv[4], pv[5]));
+      ctx->rt_ms[4] += ms;
+      HIPCHK(hipEventElapsedTime(&ms, pv[5], rt[0]));
+      ctx->rt_ms[5] += ms;
+    }
+    ctx->rt_rounds += 1;
+  }
   harvest_timing(ctx);
   ctx->rounds += 1;
 
@@ -1292,6 +1335,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     info->row_layers = row_layers;
     for (int s = 0; s < B; ++s) { info->q[s] = q_start[s]; info->kstar[s] = -1; }
     info->rounds_total = ctx->rounds;
+    info->attn_bytes = attn_bytes;
   }
   // ------------------------------------------------- commit + collapse
   int njobs = 0;
@@ -1364,6 +1408,30 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     TimedLaunch tl(ctx, 7, 0.0);
     HIPCHK(launch_collapse(c, ctx->stream));
   }
+  if (rt) {
+    HIPCHK(hipEventRecord(rt[5], ctx->stream));
+    ctx->rt_prev = true;
+    ctx->rt_cur = 1 - ctx->rt_cur;
+  }
+  return DEX_OK;
+}
+
+dex_status dex_debug_set_round_timing(dex_ctx *ctx, int32_t enable) {
+  if (!ctx) return DEX_E_INVAL;
+  for (auto &set : ctx->rt_ev)
+    for (auto &e : set)
+      if (!e && hipEventCreate(&e) != hipSuccess) { ctx->err = "hipEventCreate failed"; return DEX_E_HIP; }
+  ctx->round_timing = enable != 0;
+  ctx->rt_prev = false;
+  ctx->rt_rounds = 0;
+  for (double &v : ctx->rt_ms) v = 0.0;
+  return DEX_OK;
+}
+
+dex_status dex_debug_round_times(dex_ctx *ctx, int32_t n, double *ms, int64_t *rounds) {
+  if (!ctx || !ms || !rounds || n < 0 || n > kRoundPhases) return DEX_E_INVAL;
+  for (int i = 0; i < n; ++i) ms[i] = ctx->rt_ms[i];
+  *rounds = ctx->rt_rounds;
   return DEX_OK;
 }
 

@@ -27,6 +27,7 @@ EXPORTED = (
     "dex_debug_kv_layout", "dex_debug_slot_entry", "dex_debug_set_kernel_timing",
     "dex_debug_kernel_times", "dex_debug_time_kernel", "dex_debug_gemm", "dex_debug_attention",
     "dex_debug_gumbel", "dex_debug_copy", "dex_debug_plan", "dex_debug_attention_noalloc",
+    "dex_debug_set_round_timing", "dex_debug_round_times",
 )
 
 
@@ -67,6 +68,7 @@ class DexStepInfo(ctypes.Structure):
         ("row_pos", ctypes.c_int32 * DEX_MAX_ROWS),
         ("row_token", ctypes.c_int32 * DEX_MAX_ROWS),
         ("rounds_total", ctypes.c_int64),
+        ("attn_bytes", ctypes.c_double),
     ]
 
 
@@ -105,6 +107,8 @@ def load(path: str | None = None):
                                         P(i32), P(i32), i32, vp, vp]
     lib.dex_debug_attention_noalloc.argtypes = list(lib.dex_debug_attention.argtypes)
     lib.dex_debug_gumbel.argtypes = [ctypes.c_uint64, i32, i32, i32, vp, vp]
+    lib.dex_debug_set_round_timing.argtypes = [vp, i32]
+    lib.dex_debug_round_times.argtypes = [vp, i32, P(ctypes.c_double), P(i64)]
     lib.dex_debug_plan.argtypes = [i32, i32, i32, i32, P(i32), i32, P(i32), i32, P(i32)]
     for name in EXPORTED:
         if name not in ("dex_destroy", "dex_last_error"):
@@ -319,6 +323,17 @@ class Decoder:
         _check(self.lib, self.ctx, self.lib.dex_debug_kernel_times(self.ctx, 8, ms, n, b))
         return list(ms), list(n), list(b)
 
+    def set_round_timing(self, on: bool):
+        _check(self.lib, self.ctx, self.lib.dex_debug_set_round_timing(self.ctx, int(on)))
+
+    def round_times(self):
+        """(per-phase milliseconds summed over the timed rounds, rounds); see
+        ROUND_PHASES."""
+        ms = (ctypes.c_double * 7)()
+        n = ctypes.c_int64()
+        _check(self.lib, self.ctx, self.lib.dex_debug_round_times(self.ctx, 7, ms, ctypes.byref(n)))
+        return list(ms), n.value
+
     def time_kernel(self, cls: int, M: int, reps: int = 64):
         """(mean microseconds, algorithmic bytes) of one decode GEMM launch."""
         us, b = ctypes.c_double(), ctypes.c_double()
@@ -338,4 +353,5 @@ class Decoder:
             pass
 
 
+ROUND_PHASES = ("upload", "sweep", "exit", "copy", "commit_collapse", "gap_before_round", "host_plan")
 KERNEL_CLASSES = ("qkv", "attention", "attn_combine", "o_proj", "gate_up", "down", "lm_head", "other")

@@ -118,6 +118,26 @@ def stats(args):
         for k in sorted(groups):
             v = groups[k]
             lines.append(f"  {k:34s} launches={len(v):6d} median_us={statistics.median(v):8.2f}")
+    if args.out_json and trace:
+        # average duration of every launch of each decode GEMM class (the
+        # instantiation the benchmark's workload uses), for bench.py's
+        # roofline next to its own timing
+        cls_of = {"gemm_kernel<unsigned short, 1,": "qkv", "gemm_kernel<unsigned short, 3,": "gate_up",
+                  "gemm_kernel<unsigned short, 4,": "lm_head", "gemm_kernel<unsigned short, 2,": "o_proj+down"}
+        per = {}
+        for t in trace:
+            n = _short(t["Kernel_Name"])
+            dur = (int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e3
+            for k, c in cls_of.items():
+                if n.startswith(k):
+                    per.setdefault(c, {}).setdefault(n, []).append(dur)
+        classes = {}
+        for c, insts in per.items():
+            n, v = max(insts.items(), key=lambda kv: len(kv[1]))     # the most launched instantiation
+            classes[c] = {"kernel": n, "launches": len(v), "avg_us": statistics.fmean(v),
+                          "median_us": statistics.median(v)}
+        json.dump({"source": csrc_source_hash(), "config": args.config, "command": args.command,
+                   "classes": classes}, open(args.out_json, "w"), indent=1)
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     open(args.out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -270,6 +290,8 @@ def main():
     s.add_argument("--command", required=True)
     s.add_argument("--out", required=True)
     s.add_argument("--top", type=int, default=16)
+    s.add_argument("--out-json", default=None)
+    s.add_argument("--config", default="llama-32L-d4096-x8-w4")
     t = sub.add_parser("traffic")
     t.add_argument("fetch_dir")
     t.add_argument("write_dir")
