@@ -784,6 +784,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   A((void **)&ctx->job_dev, (size_t)(ctx->B * (ctx->S + 1)) * 6 * 4 + 256);
   ctx->tab_cap = (size_t)R * (16 + 2 * N + ctx->CH_MAX) + 4 * ctx->B + 1024;
   A((void **)&ctx->tab_dev, ctx->tab_cap * 4);
+
   if (st != DEX_OK) {
     g_create_error = ctx->err;
     dex_destroy(ctx);
@@ -808,6 +809,7 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
     if (e == hipSuccess) e = hipMemset(ctx->kc, 0, kv_bytes);
     if (e == hipSuccess) e = hipMemset(ctx->vc, 0, kv_bytes);
     if (e == hipSuccess) e = hipMemset(ctx->cand, 0xff, slots_total * N * 4);
+
     if (e != hipSuccess) {
       g_create_error = std::string("initialisation copy failed: ") + hipGetErrorString(e);
       dex_destroy(ctx);
@@ -1228,6 +1230,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   // spread over the lanes; the exit heads wait for all of them.  (Per-kernel
   // timing keeps everything on one stream.)
   const bool multi = ctx->n_lanes > 1 && !ctx->timing;
+
   if (multi) {
     HIPCHK(hipEventRecord(ctx->fork_ev, ctx->stream));
     for (int i = 1; i < ctx->n_lanes; ++i) HIPCHK(hipStreamWaitEvent(ctx->lane_st[i], ctx->fork_ev, 0));
@@ -1256,6 +1259,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     }
     t.n_splits = std::min(ctx->jmax, stage_maxpos / ATT_SPLIT + 1);
     t.attn_bytes += (double)M * ctx->H * ctx->hd * (4.0 + ctx->es);
+
     attn_bytes += t.attn_bytes * (double)ls.size();
     {
       PrepArgs p{};

@@ -25,66 +25,9 @@
 //           the slot's Gumbel noise, DECS mask (-inf), and the tile's argmax
 //           (lowest id on ties);
 //   PLAIN   float output (tests).
-#include "dex_kernels.h"
+#include "gemm_common.h"
 
 namespace dex {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
-
-__device__ __forceinline__ float bf2f(bf16 b) { return __uint_as_float(((uint32_t)b) << 16); }
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
-}
-template <typename T> __device__ __forceinline__ T to_t(float f);
-template <> __device__ __forceinline__ float to_t<float>(float f) { return f; }
-template <> __device__ __forceinline__ bf16 to_t<bf16>(float f) { return f2bf(f); }
-
-// One 16-byte fragment per lane and the MFMA steps it feeds.
-template <typename T> struct Frag;
-template <> struct Frag<bf16> {
-  u32x4_t v;
-  static constexpr int EPB = 8;           // elements per 16 bytes
-  __device__ __forceinline__ static f32x4_t mma(const Frag &a, const Frag &b, f32x4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
-                                                   __builtin_bit_cast(bf16x8_t, b.v), c, 0, 0, 0);
-  }
-};
-template <> struct Frag<float> {
-  u32x4_t v;
-  static constexpr int EPB = 4;
-  __device__ __forceinline__ static f32x4_t mma(const Frag &a, const Frag &b, f32x4_t c) {
-    // k-slot (lane group g, element e) <-> k = 4 g + e, identical for A and B
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.x), __uint_as_float(b.v.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.y), __uint_as_float(b.v.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.z), __uint_as_float(b.v.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.v.w), __uint_as_float(b.v.w), c, 0, 0, 0);
-    return c;
-  }
-};
-
-__device__ __forceinline__ u32x4_t load16(const void *p, bool ok) {
-  if (!ok) return u32x4_t{0u, 0u, 0u, 0u};
-  return __builtin_nontemporal_load((const u32x4_t *)p);
-}
-__device__ __forceinline__ u32x4_t load16_cached(const void *p, bool ok) {
-  if (!ok) return u32x4_t{0u, 0u, 0u, 0u};
-  return *(const u32x4_t *)p;
-}
-
-// RMSNorm reciprocal scale of one row from its sum-of-squares partials.  The
-// single definition used by every consumer: lane j sums partials j, j+64, ...
-// in order, then a fixed butterfly across the wave.
-__device__ __forceinline__ float row_rscale(const float *part, int n_part, float inv_d, float eps, int lane) {
-  float s = 0.f;
-  for (int t = lane; t < n_part; t += 64) s += part[t];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
-  return 1.0f / sqrtf(s * inv_d + eps);
-}
 
 // U: k-steps per prefetch chunk (two chunks in flight per wave).  It only
 // sets how far loads run ahead: every wave still accumulates its steps in
@@ -99,7 +42,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   constexpr int KSTEP = 4 * EPB;               // k covered by one 16-byte step of a wave
   constexpr int NT = (EPI == EPI_SWIGLU) ? 2 : 1;
   constexpr int NA = NT * NTW;                 // weight blocks per step of the workgroup
-  __shared__ float red[GEMM_WAVES][NA][MB][64][4];
+  __shared__ float red_all[NA][GEMM_WAVES][MB][64][4];
   __shared__ float val[NA][16][16 * MB];
   __shared__ float rs[16 * MB];
 
@@ -182,7 +125,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) red[wave][t][mb][lane][i] = acc[t][mb][i];
+      for (int i = 0; i < 4; ++i) red_all[t][wave][mb][lane][i] = acc[t][mb][i];
 
   // RMSNorm scales of this block's rows
   if (a.part != nullptr) {
@@ -192,18 +135,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
     }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < NA * MB * 256; e += GEMM_THREADS) {
-    const int t = e / (MB * 256), rem = e % (MB * 256);
-    const int mb = rem / 256, li = rem % 256;
-    const int ln = li >> 2, i = li & 3;
-    float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < GEMM_WAVES; ++w) sum += red[w][t][mb][ln][i];
-    // C layout: lane ln holds rows 4*(ln/16)+i (output columns) of column ln%16 (input rows)
-    const int nl = 4 * (ln >> 4) + i;
-    const int ml = mb * 16 + (ln & 15);
-    val[t][nl][ml] = sum;
-  }
+  for (int t = 0; t < NA; ++t) reduce_block<MB>(red_all[t], val[t]);
   __syncthreads();
 
   // ---- epilogues, one weight tile at a time
@@ -252,27 +185,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
     }
   } else if constexpr (EPI == EPI_RESID) {
     __shared__ float sq[16][16 * MB];
-    for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
-      const int ml = e / 16, nl = e % 16;
-      const int m = m0 + ml, n = tile * 16 + nl;
-      const float *hin = a.h + (size_t)m * a.ld_h;
-      float *hout = (a.row_bnd != nullptr) ? a.bnd_h + (size_t)a.row_bnd[m] * a.ld_h : a.h + (size_t)m * a.ld_h;
-      const float br = (a.bias != nullptr) ? a.alpha * (vt[0][nl][ml] + a.bias[n]) : a.alpha * vt[0][nl][ml];
-      const float hn = hin[n] + br;
-      hout[n] = hn;
-      if (a.xb != nullptr) ((T *)a.xb)[(size_t)m * a.ld_h + n] = to_t<T>(a.g_next[n] * hn);
-      sq[nl][ml] = hn * hn;
-    }
-    __syncthreads();
-    for (int ml = threadIdx.x; ml < Mloc; ml += GEMM_THREADS) {
-      const int m = m0 + ml;
-      float s = 0.f;
-#pragma unroll
-      for (int nl = 0; nl < 16; ++nl) s += sq[nl][ml];
-      float *po = (a.row_bnd != nullptr) ? a.bnd_part + (size_t)a.row_bnd[m] * a.n_part_out
-                                         : a.part_out + (size_t)m * a.n_part_out;
-      po[tile] = s;
-    }
+    epi_resid<T, MB>(a, tile, m0, Mloc, vt[0], sq);
   } else if constexpr (EPI == EPI_SWIGLU) {
     for (int e = threadIdx.x; e < 16 * Mloc; e += GEMM_THREADS) {
       const int ml = e / 16, nl = e % 16;
