@@ -119,3 +119,28 @@ def test_copy_kernel():
     assert lib.dex_debug_copy(b.data_ptr(), a.data_ptr(), a.numel() * 4, None) == 0
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("dtype", [1, 0])
+def test_weight_row_bits_do_not_depend_on_its_tile(dtype):
+    """A weight row's outputs have the same bits whatever the other rows of
+    its 16-row tile hold (zeros, other rows, the row itself moved to another
+    tile and position): the matrix cores give each output element its own
+    row's dot product.  (With the activation-row independence above, this is
+    what lets the workgroup tiling of a GEMM change without changing a
+    bit.)"""
+    torch = torch_cuda()
+    N, K = 64, 4096 if dtype == 1 else 344
+    for M in (1, 7, 16):
+        Wt, xt, _, _ = _inputs(torch, dtype, N, K, M, 500 + M)
+        y = _gemm(torch, dtype, Wt, xt, M)
+        rng = np.random.default_rng(M)
+        perm = rng.permutation(N)
+        y_perm = _gemm(torch, dtype, Wt[torch.from_numpy(perm).cuda()].contiguous(), xt, M)
+        assert np.array_equal(y_perm.view(np.uint32), y[:, perm].view(np.uint32))
+        keep = np.zeros(N, dtype=bool)
+        keep[rng.choice(N, size=N // 3, replace=False)] = True
+        Wz = Wt.clone()
+        Wz[torch.from_numpy(~keep).cuda()] = 0
+        y_z = _gemm(torch, dtype, Wz, xt, M)
+        assert np.array_equal(y_z[:, keep].view(np.uint32), y[:, keep].view(np.uint32))
