@@ -205,12 +205,13 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int g = 0; g < GMAX; ++g) {
       if (g >= G) break;
-      float *dst = a.part + (((size_t)r * a.n_heads + kvh * G + g) * a.jmax + split) * (HD + 2);
+      const size_t rec = ((size_t)r * a.n_heads + kvh * G + g) * a.jmax + split;
+      float *dst = a.part + rec * HD;
       if (dims_ok) {
 #pragma unroll
         for (int q = 0; q < DPL; ++q) dst[d0 + q] = o[g][q];
       }
-      if (lane == 0) { dst[HD] = m[g]; dst[HD + 1] = l[g]; }
+      if (lane == 0) { a.stat[2 * rec] = m[g]; a.stat[2 * rec + 1] = l[g]; }
     }
   }
 
@@ -240,7 +241,8 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   const int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, s = tid >> 6;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
   const int nmine = nsplit > s ? (nsplit - s + CMB_WAVES - 1) / CMB_WAVES : 0;
-  const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * (HD + 2);
+  const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * HD;
+  const float *sst = a.stat + ((size_t)r * a.n_heads + h) * a.jmax * 2;
   const int dl = lane * DPL;                   // this lane's first dimension in the slice
   const int d0 = blockIdx.z * DW + dl;
   const bool dok = dl < DW;
@@ -253,12 +255,12 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
       const int j = s + (i0 + jj) * CMB_WAVES;
 #pragma unroll
       for (int q = 0; q < DPL; ++q)
-        v[jj][q] = (dok && i0 + jj < nmine) ? src[(size_t)j * (HD + 2) + d0 + q] : 0.f;
+        v[jj][q] = (dok && i0 + jj < nmine) ? src[(size_t)j * HD + d0 + q] : 0.f;
     }
   };
   load_chunk(0, va);
   float M = -INFINITY;
-  for (int j = tid; j < nsplit; j += NT) M = fmaxf(M, src[(size_t)j * (HD + 2) + HD]);
+  for (int j = tid; j < nsplit; j += NT) M = fmaxf(M, sst[2 * j]);
   M = wave_max(M);
   if (lane == 0) sred[0][s] = M;
   __syncthreads();
@@ -267,9 +269,9 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   for (int w = 1; w < CMB_WAVES; ++w) M = fmaxf(M, sred[0][w]);
   float lp = 0.f;
   for (int j = tid; j < nsplit; j += NT) {
-    const float w = expf(src[(size_t)j * (HD + 2) + HD] - M);
+    const float w = expf(sst[2 * j] - M);
     ws[j] = w;
-    lp = fmaf(w, src[(size_t)j * (HD + 2) + HD + 1], lp);
+    lp = fmaf(w, sst[2 * j + 1], lp);
   }
   lp = wave_sum(lp);
   if (lane == 0) sred[1][s] = lp;

@@ -47,11 +47,16 @@ __device__ __forceinline__ void wave_lds_sync() {
 //   S^T = K Q^T  the split's four 16-key tiles against the (row, query
 //                head) pairs as 16 columns, q rounded to bf16: each lane
 //                then holds 16 keys of one pair;
-//   O = P V      P = exp(S - max) rounded to bf16 straight from those
-//                accumulators (the k-slots of the A operand are ordered as
-//                the keys the lane holds), V staged row-major in LDS and
-//                read back in the same key order through the transpose
-//                read (tr_frag).
+//   O^T = V^T P^T  P = exp(S - max) rounded to bf16 straight from those
+//                accumulators (the B operand's k-slots are ordered as the
+//                keys the lane holds), V staged row-major in LDS and read
+//                back in the same key order through the transpose read
+//                (tr_frag) as the A operand; each lane then holds four
+//                consecutive dimensions of its own pair per 16-dimension
+//                tile and writes them with one 16-byte store.  (The same
+//                registers as an O = P V product with the operands swapped:
+//                the output bits are the same, and the split record needs
+//                8 vector stores per lane instead of 32 scalar ones.)
 // Keys are loaded in fragment order (16 keys x 64 bytes per instruction),
 // values as whole key rows (four per instruction): value loads of one key
 // row per lane touch 64 cache lines per instruction and held the split's
@@ -257,14 +262,17 @@ __device__ void attn_mfma_item(const AttnArgs &a, int item, int kvh, uint16_t (*
       }
     sum += __shfl_xor(sum, 16, 64);
     sum += __shfl_xor(sum, 32, 64);
+    // O^T = V^T P^T: the transpose reads of V (the A operand) and the P
+    // fragment (B) are the registers an O = P V product would use, swapped,
+    // so each lane holds four consecutive dimensions of its own pair pa
     pf_f32x4 o[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = pf_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < ATT_SPLIT / 32; ++st) {
-      // A = P (pairs x 32 keys): k-slot e of lane (pair r16, grp) is key
+      // P^T (32 keys x pairs): k-slot e of lane (pair r16, grp) is key
       // 32 st + 4 grp + e (e < 4) or 32 st + 16 + 4 grp + e - 4, exactly the
-      // S^T values this lane holds; the V operand uses the same key order
+      // S^T values this lane holds; V^T's k-slots follow the same key order
       const pf_bf16x8 pfr = __builtin_bit_cast(
           pf_bf16x8, make_uint4(pf_pack_bf16(sc[2 * st][0], sc[2 * st][1]), pf_pack_bf16(sc[2 * st][2], sc[2 * st][3]),
                                 pf_pack_bf16(sc[2 * st + 1][0], sc[2 * st + 1][1]),
@@ -272,25 +280,17 @@ __device__ void attn_mfma_item(const AttnArgs &a, int item, int kvh, uint16_t (*
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            pfr,
             tr_frag(&vr[32 * st + 4 * tq + ti][16 * dt + 4 * tg], &vr[32 * st + 16 + 4 * tq + ti][16 * dt + 4 * tg]),
-            o[dt], 0, 0, 0);
+            pfr, o[dt], 0, 0, 0);
     }
-    // statistics of pair pa from its first quarter
-    if (pok && grp == 0) {
-      float *dst = a.part + (((size_t)(r0 + prow[pa / G]) * a.n_heads + kvh * G + pa % G) * a.jmax + split) * (HD + 2);
-      dst[HD] = mx;
-      dst[HD + 1] = sum;
-    }
-    // partials: lane holds O[pair mt*16 + 4 grp + i][dim 16 dt + r16]
+    // pair pa's record: O[pa][16 dt + 4 grp .. + 3] as one 16-byte store per
+    // tile, and its statistics from the first quarter
+    if (pok) {
+      const size_t rec = ((size_t)(r0 + prow[pa / G]) * a.n_heads + kvh * G + pa % G) * a.jmax + split;
+      float *dst = a.part + rec * HD + 4 * grp;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int pc = mt * 16 + grp * 4 + i;
-      if (pc >= P) continue;
-      const int prw = r0 + prow[pc / G];
-      float *dst = a.part + (((size_t)prw * a.n_heads + kvh * G + pc % G) * a.jmax + split) * (HD + 2);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) dst[dt * 16 + r16] = o[dt][i];
+      for (int dt = 0; dt < DT; ++dt) *(pf_f32x4 *)(dst + 16 * dt) = o[dt];
+      if (grp == 0) *(float2 *)(a.stat + 2 * rec) = make_float2(mx, sum);
     }
   }
 }

@@ -119,6 +119,13 @@ struct GemmArgs {
   unsigned long long sample_seed;
 };
 
+// Split partials of R rows live in one buffer of R * H * jmax * (hd + 2)
+// floats: the outputs o ([R][H][jmax][hd], whole 128-byte lines per record
+// at hd 32..128) and then the statistics ([R][H][jmax] of (max, sum)).
+inline float *split_stats(float *part, size_t rows, int n_heads, int jmax, int hd) {
+  return part + rows * n_heads * jmax * hd;
+}
+
 struct AttnArgs {
   const float *q;             // [R][H*hd], RoPE applied
   int ldq;
@@ -129,14 +136,15 @@ struct AttnArgs {
   const int *row_pos, *row_nc, *row_chain_off, *chain;
   const int *row_seq;         // sequence of each row (matrix-core kernel)
   int n_rows;                 // rows of the launch (matrix-core kernel)
-  float *part;                // [R][H][jmax][hd + 2] split partials (o, max, sum)
-  int jmax;                   // split stride of `part`
+  float *part;                // [R][H][jmax][hd] split partial outputs o
+  float *stat;                // [R][H][jmax][2] their (max, sum)
+  int jmax;                   // split stride of `part` and `stat`
   int n_splits;               // splits the launch covers: max over its rows of pos / 64 + 1 (<= jmax)
   float scale;
 };
 
 struct CombineArgs {
-  const float *part;
+  const float *part, *stat;   // as AttnArgs
   const int *row_pos;
   int jmax, n_heads, head_dim;
   void *out;                  // [R][H*hd] (T)

@@ -369,13 +369,15 @@ dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_la
       a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq;
       a.row_pos = t.pos; a.row_nc = t.nc; a.row_chain_off = t.chain_off; a.chain = t.chain;
       a.row_seq = t.seq; a.n_rows = M;
-      a.part = apart; a.jmax = jmax; a.n_splits = t.n_splits; a.scale = 1.0f / std::sqrt((float)hd);
+      a.part = apart; a.stat = split_stats(apart, M, H, jmax, hd);
+      a.jmax = jmax; a.n_splits = t.n_splits; a.scale = 1.0f / std::sqrt((float)hd);
       TimedLaunch tl(ctx, 1, t.attn_bytes);
       HIPCHK(launch_attention(ctx->dtype, a, t.n_groups, st));
     }
     {
       CombineArgs c{};
-      c.part = apart; c.row_pos = t.pos; c.jmax = jmax; c.n_heads = H; c.head_dim = hd;
+      c.part = apart; c.stat = split_stats(apart, M, H, jmax, hd);
+      c.row_pos = t.pos; c.jmax = jmax; c.n_heads = H; c.head_dim = hd;
       c.out = att; c.ld_out = H * hd;
       TimedLaunch tl(ctx, 2, 0.0);
       HIPCHK(launch_combine(ctx->dtype, c, M, st));
@@ -612,10 +614,11 @@ hipError_t launch_attention_call(const AttnCall &c, const AttnTab &t, const int 
   a.grp_row0 = dtab + t.o_g0; a.grp_nrows = dtab + t.o_gn; a.grp_seq = dtab + t.o_gs;
   a.row_pos = dtab + t.o_pos; a.row_nc = dtab + t.o_nc; a.row_chain_off = dtab + t.o_coff;
   a.chain = dtab + t.o_chain; a.row_seq = dtab + t.o_seq; a.n_rows = c.n_rows; a.part = part;
+  a.stat = split_stats(part, c.n_rows, c.n_heads, t.n_splits, c.head_dim);
   a.jmax = t.n_splits; a.n_splits = t.n_splits; a.scale = 1.0f / std::sqrt((float)c.head_dim);
   hipError_t e = launch_attention(c.dtype, a, t.ng, st);
   CombineArgs cb{};
-  cb.part = part; cb.row_pos = dtab + t.o_pos; cb.jmax = t.n_splits; cb.n_heads = c.n_heads;
+  cb.part = part; cb.stat = a.stat; cb.row_pos = dtab + t.o_pos; cb.jmax = t.n_splits; cb.n_heads = c.n_heads;
   cb.head_dim = c.head_dim; cb.out = c.out; cb.ld_out = c.n_heads * c.head_dim;
   if (e == hipSuccess) e = launch_combine(c.dtype, cb, c.n_rows, st);
   return e;
@@ -1042,10 +1045,12 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
       a.grp_row0 = d_grel + g_first; a.grp_nrows = d_gn + g_first; a.grp_seq = d_gs + g_first;
       a.row_pos = d_pos + c0; a.row_nc = d_nc + c0; a.row_chain_off = d_coff + c0; a.chain = d_zero;
       a.row_seq = d_seq + c0; a.n_rows = cn;
-      a.part = apart; a.jmax = jmax; a.n_splits = jmax; a.scale = 1.0f / std::sqrt((float)hd);
+      a.part = apart; a.stat = split_stats(apart, cn, H, jmax, hd);
+      a.jmax = jmax; a.n_splits = jmax; a.scale = 1.0f / std::sqrt((float)hd);
       HIPCHK(launch_attention(ctx->dtype, a, g_cnt, ctx->stream));
       CombineArgs cb{};
-      cb.part = apart; cb.row_pos = d_pos + c0; cb.jmax = jmax; cb.n_heads = H; cb.head_dim = hd;
+      cb.part = apart; cb.stat = split_stats(apart, cn, H, jmax, hd);
+      cb.row_pos = d_pos + c0; cb.jmax = jmax; cb.n_heads = H; cb.head_dim = hd;
       cb.out = (char *)att + (size_t)c0 * H * hd * es; cb.ld_out = H * hd;
       HIPCHK(launch_combine(ctx->dtype, cb, cn, ctx->stream));
     }

@@ -313,16 +313,23 @@ static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
   } else {
     // more rows: the wide matrices take several weight tiles per workgroup
     // so that each activation load feeds them all -- four for the 2000-tile
-    // LM head, two for gate/up; the 256/384-tile projections keep one tile
-    // per workgroup to fill the chip (measured per class at 24-64 rows); with
-    // 64-row blocks the reduction buffer takes most of the LDS
+    // LM head and for gate/up up to 32 rows, two for gate/up beyond; the
+    // 256-tile projections take two tiles per workgroup and split the rows
+    // over a second grid row from 25 rows on (the same 256 workgroups, each
+    // activation load feeding two tiles); the 384-tile QKV keeps one tile
+    // per workgroup (measured per class at 17-64 rows); with 64-row blocks
+    // the reduction buffer takes most of the LDS
     if (a.M <= 32) {
-      if constexpr (EPI == EPI_LOGITS)
+      if constexpr (EPI == EPI_LOGITS || EPI == EPI_SWIGLU)
         hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 2, 4>), dim3((n_tiles + 3) / 4, 1), block, 0, s, a);
-      else if constexpr (EPI == EPI_SWIGLU)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
+      else if (n_tiles <= 256 && a.M > 24)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 2>), dim3((n_tiles + 1) / 2, 2), block, 0, s, a);
+      else if (n_tiles <= 256)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
       else
         hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    } else if (n_tiles <= 256 && EPI != EPI_LOGITS && EPI != EPI_SWIGLU) {
+      hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, (a.M + 31) / 32), block, 0, s, a);
     } else {
       const unsigned mb = (unsigned)((a.M + 63) / 64);
       if constexpr (EPI == EPI_LOGITS)
