@@ -22,8 +22,8 @@ Prints one JSON line.  Besides the contract fields it carries
                the attention's key/value reads) times the counted/algorithmic
                ratio that rocprofv3 measured over whole decode rounds of the
                same workload (FETCH_SIZE + WRITE_SIZE, profiles/
-               step_traffic.json, only while the kernel and engine sources
-               are unchanged), over this run's time per round;
+               step_traffic_<workload>.json, only while the kernel and
+               engine sources are unchanged), over this run's time per round;
   cpu_baseline the oracle (float64 numpy) running the same decode on the host
                cores for a bounded sample, DEX and plain AR timed separately.
 """
@@ -61,8 +61,10 @@ def parse():
     p.add_argument("--adapter-alpha", type=float, default=None,
                    help="attach synthetic inducing adapters with this gate to the non-final depths")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
-    p.add_argument("--step-traffic-json", default=os.path.join(ROOT, "profiles", "step_traffic.json"))
-    p.add_argument("--kernel-stats-json", default=os.path.join(ROOT, "profiles", "kernel_stats.json"))
+    p.add_argument("--step-traffic-json", default=None,
+                   help="default: profiles/step_traffic_<workload>.json")
+    p.add_argument("--kernel-stats-json", default=None,
+                   help="default: profiles/kernel_stats_<workload>.json")
     return p.parse_args()
 
 
@@ -119,6 +121,10 @@ def main():
     from paper_2606_29223_amd import dexlib
 
     cfg = configs.get(args.config)
+    if args.step_traffic_json is None:
+        args.step_traffic_json = os.path.join(ROOT, "profiles", f"step_traffic_{cfg['name']}.json")
+    if args.kernel_stats_json is None:
+        args.kernel_stats_json = os.path.join(ROOT, "profiles", f"kernel_stats_{cfg['name']}.json")
     t0 = time.time()
     weights = gen.generate_model(cfg)
     prompts = gen.prompts(cfg)
