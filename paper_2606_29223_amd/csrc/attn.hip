@@ -40,6 +40,32 @@ template <> __device__ __forceinline__ float unpack<bf16>(const uint32_t *w, int
 }
 template <> __device__ __forceinline__ float unpack<float>(const uint32_t *w, int e) { return __uint_as_float(w[e]); }
 
+// A split record element: the split's normalised output in the cache's
+// element type (bf16 rounded to nearest even).
+template <typename T> __device__ __forceinline__ T rec_elem(float v);
+template <> __device__ __forceinline__ float rec_elem<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 rec_elem<bf16>(float v) { return pf_f2bf(v); }
+template <typename T> __device__ __forceinline__ float rec_val(T v);
+template <> __device__ __forceinline__ float rec_val<float>(float v) { return v; }
+template <> __device__ __forceinline__ float rec_val<bf16>(bf16 v) { return __uint_as_float((uint32_t)v << 16); }
+
+// DPL consecutive record elements (one load) as floats; zeros if !ok.
+template <typename T, int DPL>
+__device__ __forceinline__ void rec_load(const T *p, bool ok, float (&v)[DPL]) {
+  if constexpr (DPL == 2 && sizeof(T) == 2) {
+    const uint32_t u = ok ? *(const uint32_t *)p : 0u;
+    v[0] = __uint_as_float(u << 16);
+    v[1] = __uint_as_float(u & 0xffff0000u);
+  } else if constexpr (DPL == 2) {
+    const float2 f = ok ? *(const float2 *)p : make_float2(0.f, 0.f);
+    v[0] = f.x;
+    v[1] = f.y;
+  } else {
+#pragma unroll
+    for (int q = 0; q < DPL; ++q) v[q] = ok ? rec_val<T>(p[q]) : 0.f;
+  }
+}
+
 // One wave per (row group, kv head, split of 64 logical keys).  Lane i owns
 // key s0 + i for the scores and head dimensions [i*DPL, i*DPL + DPL) for the
 // value sum.
@@ -206,10 +232,11 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
     for (int g = 0; g < GMAX; ++g) {
       if (g >= G) break;
       const size_t rec = ((size_t)r * a.n_heads + kvh * G + g) * a.jmax + split;
-      float *dst = a.part + rec * HD;
+      T *dst = (T *)a.part + rec * HD;
+      const float inv = l[g] > 0.f ? 1.f / l[g] : 0.f;
       if (dims_ok) {
 #pragma unroll
-        for (int q = 0; q < DPL; ++q) dst[d0 + q] = o[g][q];
+        for (int q = 0; q < DPL; ++q) dst[d0 + q] = rec_elem<T>(o[g][q] * inv);
       }
       if (lane == 0) { a.stat[2 * rec] = m[g]; a.stat[2 * rec + 1] = l[g]; }
     }
@@ -217,8 +244,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 
 }
 
-// out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M}, M = max_j m_j,
-// over the splits j = 0 .. pos/64 of row r.  One workgroup of CMB_WAVES
+// out[r][h] = sum_j c_j (o_j / l_j) / sum_j c_j with c_j = e^{m_j - M} l_j,
+// M = max_j m_j, over the splits j = 0 .. pos/64 of row r (each split
+// record holds its normalised output o_j / l_j and its (m_j, l_j)).  One workgroup of CMB_WAVES
 // waves per (row, head): wave s sums the splits j = s, s + CMB_WAVES, ... in
 // order (lanes over head dimensions) and the wave sums are added in wave
 // order; the statistics take one fixed reduction.  The arithmetic depends
@@ -232,7 +260,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 #endif
 template <typename T, int HD, int DW>
 __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) {
-  constexpr int DPL = DW >= 64 ? DW / 64 : 1;
+  // dimensions per lane: 4-byte record loads for bf16 (whole heads: 64
+  // lanes x 2; half heads: 32 lanes x 2)
+  constexpr int DPL = sizeof(T) == 2 ? (DW >= 128 ? DW / 64 : 2) : (DW >= 64 ? DW / 64 : 1);
   constexpr int CH = 16;                       // splits per value chunk
   constexpr int NT = 64 * CMB_WAVES;
   extern __shared__ float ws[];                // [jmax] split weights
@@ -241,7 +271,7 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   const int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, s = tid >> 6;
   const int nsplit = a.row_pos[r] / ATT_SPLIT + 1;
   const int nmine = nsplit > s ? (nsplit - s + CMB_WAVES - 1) / CMB_WAVES : 0;
-  const float *src = a.part + ((size_t)r * a.n_heads + h) * a.jmax * HD;
+  const T *src = (const T *)a.part + ((size_t)r * a.n_heads + h) * a.jmax * HD;
   const float *sst = a.stat + ((size_t)r * a.n_heads + h) * a.jmax * 2;
   const int dl = lane * DPL;                   // this lane's first dimension in the slice
   const int d0 = blockIdx.z * DW + dl;
@@ -253,9 +283,7 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
 #pragma unroll
     for (int jj = 0; jj < CH; ++jj) {
       const int j = s + (i0 + jj) * CMB_WAVES;
-#pragma unroll
-      for (int q = 0; q < DPL; ++q)
-        v[jj][q] = (dok && i0 + jj < nmine) ? src[(size_t)j * HD + d0 + q] : 0.f;
+      rec_load<T, DPL>(src + (size_t)j * HD + d0, dok && i0 + jj < nmine, v[jj]);
     }
   };
   load_chunk(0, va);
@@ -269,9 +297,9 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   for (int w = 1; w < CMB_WAVES; ++w) M = fmaxf(M, sred[0][w]);
   float lp = 0.f;
   for (int j = tid; j < nsplit; j += NT) {
-    const float w = expf(sst[2 * j] - M);
+    const float w = expf(sst[2 * j] - M) * sst[2 * j + 1];
     ws[j] = w;
-    lp = fmaf(w, sst[2 * j + 1], lp);
+    lp += w;
   }
   lp = wave_sum(lp);
   if (lane == 0) sred[1][s] = lp;
