@@ -182,3 +182,20 @@ def test_attention_rows_do_not_depend_on_the_launch(dtype, hd, H, Hkv):
     _, part = _run(torch, c, sub)
     for i, r in enumerate(sub):
         assert np.array_equal(part[i], full[r]), r
+
+
+@pytest.mark.parametrize("dtype,hd,H,Hkv", [(1, 128, 32, 8), (1, 64, 12, 12), (0, 32, 4, 4)])
+def test_short_rows_same_bits_beside_a_long_row(dtype, hd, H, Hkv):
+    """Short rows (at most 64 splits) get the same bits alone and in a launch
+    that also holds a 71-split row (more split items, the long row setting
+    the launch's split count)."""
+    torch = torch_cuda()
+    c = Case(dtype, hd, H, Hkv, LATTICE + [(4500, [1, 2])], seed=29)
+    short = [r for r in range(c.R) if c.pos[r] // 64 + 1 <= 64]
+    assert len(short) < c.R
+    _, mixed = _run(torch, c)
+    _, alone = _run(torch, c, short)
+    for i, r in enumerate(short):
+        assert np.array_equal(alone[i], mixed[r]), r
+    got, _ = _run(torch, c)
+    _check(c, got, c.reference(), BF16_RTOL if dtype == 1 else F32_RTOL)
