@@ -40,8 +40,8 @@ template <> __device__ __forceinline__ float unpack<bf16>(const uint32_t *w, int
 }
 template <> __device__ __forceinline__ float unpack<float>(const uint32_t *w, int e) { return __uint_as_float(w[e]); }
 
-// A split record element: the split's normalised output in the cache's
-// element type (bf16 rounded to nearest even).
+// A split record element: the split's output in the cache's element type
+// (bf16 rounded to nearest even).
 template <typename T> __device__ __forceinline__ T rec_elem(float v);
 template <> __device__ __forceinline__ float rec_elem<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16 rec_elem<bf16>(float v) { return pf_f2bf(v); }
@@ -233,10 +233,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
       if (g >= G) break;
       const size_t rec = ((size_t)r * a.n_heads + kvh * G + g) * a.jmax + split;
       T *dst = (T *)a.part + rec * HD;
-      const float inv = l[g] > 0.f ? 1.f / l[g] : 0.f;
       if (dims_ok) {
 #pragma unroll
-        for (int q = 0; q < DPL; ++q) dst[d0 + q] = rec_elem<T>(o[g][q] * inv);
+        for (int q = 0; q < DPL; ++q) dst[d0 + q] = rec_elem<T>(o[g][q]);
       }
       if (lane == 0) { a.stat[2 * rec] = m[g]; a.stat[2 * rec + 1] = l[g]; }
     }
@@ -244,9 +243,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 
 }
 
-// out[r][h] = sum_j c_j (o_j / l_j) / sum_j c_j with c_j = e^{m_j - M} l_j,
-// M = max_j m_j, over the splits j = 0 .. pos/64 of row r (each split
-// record holds its normalised output o_j / l_j and its (m_j, l_j)).  One workgroup of CMB_WAVES
+// out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M}, M = max_j m_j,
+// over the splits j = 0 .. pos/64 of row r (each split record holds its
+// output o_j, in the cache's element type, and its float (m_j, l_j)).  One workgroup of CMB_WAVES
 // waves per (row, head): wave s sums the splits j = s, s + CMB_WAVES, ... in
 // order (lanes over head dimensions) and the wave sums are added in wave
 // order; the statistics take one fixed reduction.  The arithmetic depends
@@ -297,9 +296,9 @@ __global__ __launch_bounds__(64 * CMB_WAVES) void combine_kernel(CombineArgs a) 
   for (int w = 1; w < CMB_WAVES; ++w) M = fmaxf(M, sred[0][w]);
   float lp = 0.f;
   for (int j = tid; j < nsplit; j += NT) {
-    const float w = expf(sst[2 * j] - M) * sst[2 * j + 1];
+    const float w = expf(sst[2 * j] - M);
     ws[j] = w;
-    lp += w;
+    lp = fmaf(w, sst[2 * j + 1], lp);
   }
   lp = wave_sum(lp);
   if (lane == 0) sred[1][s] = lp;

@@ -42,8 +42,8 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 // Decode attention on the matrix cores (bf16 caches, head_dim 64 or 128).
 //
-// Same partials as attn_kernel -- (o / sum, max, sum) per (row, query head,
-// split of 64 logical keys) -- with the two products on v_mfma_f32_16x16x32_bf16:
+// Same partials as attn_kernel -- (o, max, sum) per (row, query head, split
+// of 64 logical keys) -- with the two products on v_mfma_f32_16x16x32_bf16:
 //   S^T = K Q^T  the split's four 16-key tiles against the (row, query
 //                head) pairs as 16 columns, q rounded to bf16: each lane
 //                then holds 16 keys of one pair;
@@ -53,8 +53,8 @@ __device__ __forceinline__ void wave_lds_sync() {
 //                back in the same key order through the transpose read
 //                (tr_frag) as the A operand; each lane then holds four
 //                consecutive dimensions of its own pair per 16-dimension
-//                tile and writes them, divided by the pair's sum and
-//                rounded to bf16, with one 8-byte store.  (The same
+//                tile and writes them, rounded to bf16, with one 8-byte
+//                store.  (The same
 //                registers as an O = P V product with the operands swapped:
 //                the product's bits are the same, and the split record needs
 //                8 vector stores per lane instead of 32 scalar ones.)
@@ -284,17 +284,14 @@ __device__ void attn_mfma_item(const AttnArgs &a, int item, int kvh, uint16_t (*
             tr_frag(&vr[32 * st + 4 * tq + ti][16 * dt + 4 * tg], &vr[32 * st + 16 + 4 * tq + ti][16 * dt + 4 * tg]),
             pfr, o[dt], 0, 0, 0);
     }
-    // pair pa's record: O[pa][16 dt + 4 grp .. + 3] / sum rounded to bf16,
-    // one 8-byte store per tile, and its statistics from the first quarter
-    // (sum >= 1: the split's largest score is the pair's own maximum)
+    // pair pa's record: O[pa][16 dt + 4 grp .. + 3] rounded to bf16, one
+    // 8-byte store per tile, and its statistics from the first quarter
     if (pok) {
       const size_t rec = ((size_t)(r0 + prow[pa / G]) * a.n_heads + kvh * G + pa % G) * a.jmax + split;
       uint16_t *dst = (uint16_t *)a.part + rec * HD + 4 * grp;
-      const float inv = 1.f / sum;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        *(uint2 *)(dst + 16 * dt) = make_uint2(pf_pack_bf16(o[dt][0] * inv, o[dt][1] * inv),
-                                               pf_pack_bf16(o[dt][2] * inv, o[dt][3] * inv));
+        *(uint2 *)(dst + 16 * dt) = make_uint2(pf_pack_bf16(o[dt][0], o[dt][1]), pf_pack_bf16(o[dt][2], o[dt][3]));
       if (grp == 0) *(float2 *)(a.stat + 2 * rec) = make_float2(mx, sum);
     }
   }

@@ -120,10 +120,9 @@ struct GemmArgs {
 };
 
 // Split partials of R rows live in one buffer of R * H * jmax * (hd + 2)
-// floats: the split outputs normalised by their own sum, o / sum, in the
-// cache's element type ([R][H][jmax][hd], filling at most the first
-// R * H * jmax * hd floats), then the statistics ([R][H][jmax] of float
-// (max, sum)) at float offset R * H * jmax * hd.
+// floats: the split outputs o in the cache's element type ([R][H][jmax][hd],
+// filling at most the first R * H * jmax * hd floats), then the statistics
+// ([R][H][jmax] of float (max, sum)) at float offset R * H * jmax * hd.
 inline float *split_stats(float *part, size_t rows, int n_heads, int jmax, int hd) {
   return part + rows * n_heads * jmax * hd;
 }
@@ -138,7 +137,7 @@ struct AttnArgs {
   const int *row_pos, *row_nc, *row_chain_off, *chain;
   const int *row_seq;         // sequence of each row (matrix-core kernel)
   int n_rows;                 // rows of the launch (matrix-core kernel)
-  void *part;                 // [R][H][jmax][hd] split outputs o / sum (element type of the cache)
+  void *part;                 // [R][H][jmax][hd] split outputs o (element type of the cache)
   float *stat;                // [R][H][jmax][2] their (max, sum)
   int jmax;                   // split stride of `part` and `stat`
   int n_splits;               // splits the launch covers: max over its rows of pos / 64 + 1 (<= jmax)
