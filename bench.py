@@ -134,7 +134,10 @@ def main():
 
     P = cfg["prompt_len"]
     max_ctx = P + cfg["gen_len"]
-    need = args.warmup + 2 * args.steps + 2
+    # warm-up, the timed steps, the round-timing pass and the instrumented
+    # pass all decode on the same context (at most one commit per sequence
+    # and round)
+    need = args.warmup + 3 * args.steps + 2
     if need > cfg["gen_len"]:
         max_ctx = P + need
 
