@@ -243,9 +243,10 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 
 }
 
-// out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M}, M = max_j m_j,
-// over the splits j = 0 .. pos/64 of row r (each split record holds its
-// output o_j, in the cache's element type, and its float (m_j, l_j)).  One workgroup of CMB_WAVES
+// out[r][h] = sum_j w_j o_j / sum_j w_j l_j with w_j = e^{m_j - M},
+// M = max_j m_j, over the splits j = 0 .. pos/64 of row r (each split record
+// holds its output o_j, in the cache's element type, and its float
+// (m_j, l_j)).  One workgroup of CMB_WAVES
 // waves per (row, head): wave s sums the splits j = s, s + CMB_WAVES, ... in
 // order (lanes over head dimensions) and the wave sums are added in wave
 // order; the statistics take one fixed reduction.  The arithmetic depends
