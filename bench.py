@@ -31,6 +31,7 @@ Prints one JSON line.  Besides the contract fields it carries
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -162,28 +163,42 @@ def main():
 
     attn_total = [0.0]  # algorithmic bytes of the attention launches
 
-    def steps(n):
-        commits = rounds = layers = row_layers = 0
-        for _ in range(n):
-            c = dec.step()
-            commits += int((c >= 0).sum())
+    def run(n):
+        """n rounds; each round's commits and step info are copied out and
+        tallied after the loop, so the timed loop holds only the steps."""
+        outs = np.empty((n, B), np.int32)
+        infos = (dexlib.DexStepInfo * n)()
+        size = ctypes.sizeof(dexlib.DexStepInfo)
+        src = ctypes.addressof(dec.info)
+        for i in range(n):
+            outs[i] = dec.step()
+            ctypes.memmove(ctypes.addressof(infos[i]), src, size)
+        return outs, infos
+
+    def tally(outs, infos):
+        commits = int((outs >= 0).sum())
+        rounds = layers = row_layers = 0
+        for inf in infos:
             rounds += 1
-            layers += dec.info.layers_streamed
-            row_layers += dec.info.row_layers
-            attn_total[0] += dec.info.attn_bytes
-            ns = sum(1 for k in range(dec.N) if dec.info.rows_per_stage[k])
+            layers += inf.layers_streamed
+            row_layers += inf.row_layers
+            attn_total[0] += inf.attn_bytes
+            ns = sum(1 for k in range(dec.N) if inf.rows_per_stage[k])
             stages_hist[ns] = stages_hist.get(ns, 0) + 1
             for k in range(dec.N):
-                mk = dec.info.rows_per_stage[k]
+                mk = inf.rows_per_stage[k]
                 if mk:
                     m_hist[mk] = m_hist.get(mk, 0) + 1
                     if k < dec.N - 1:
                         ad_runs[0] += 1
             for b in range(B):
-                ks = dec.info.kstar[b]
+                ks = inf.kstar[b]
                 if ks >= 0:
                     kstar_hist[ks] = kstar_hist.get(ks, 0) + 1
         return commits, rounds, layers, row_layers
+
+    def steps(n):
+        return tally(*run(n))
 
     tw = time.perf_counter()
     warm_commits = steps(args.warmup)[0]
@@ -194,10 +209,12 @@ def main():
     stages_hist.clear()
     ad_runs[0] = 0
     attn_total[0] = 0.0
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    commits, rounds, layers, row_layers = steps(args.steps)
+    timed = run(args.steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    commits, rounds, layers, row_layers = tally(*timed)
     value = commits / elapsed
     # end to end as the paper counts it: y_0 of every sequence from the
     # prefill plus every commit, over prefill and all decode rounds so far
