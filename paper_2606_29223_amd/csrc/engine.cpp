@@ -21,8 +21,13 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
+#include <condition_variable>
+#include <functional>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "dex.h"
@@ -110,6 +115,19 @@ struct dex_ctx {
   std::vector<hipStream_t> lane_st;
   std::vector<hipEvent_t> lane_ev;
   hipEvent_t fork_ev = nullptr;
+  // lane workers, for models whose kernels take about as long as the host
+  // takes to issue a launch (~2.5 us): lanes 1.. enqueue their stages from
+  // host threads of their own while the calling thread enqueues lane 0's
+  int device = 0;
+  std::vector<std::thread> lane_threads;
+  std::atomic<int64_t> lane_ticket{0};           // round handed to the workers
+  std::atomic<bool> lane_stop{false};
+  std::unique_ptr<std::atomic<int64_t>[]> lane_done;  // per lane: last round enqueued
+  std::vector<dex_status> lane_status;
+  std::vector<std::string> lane_err;
+  std::function<dex_status(int)> lane_fn;        // the round's work of a lane
+  std::mutex lane_mu;
+  std::condition_variable lane_cv;
   std::vector<std::vector<int>> stage_layers;
   // capacities
   int S, R_max, CH_MAX, E, n_part, jmax;
@@ -142,7 +160,8 @@ struct dex_ctx {
   int *tab_host = nullptr, *res_host = nullptr, *job_host = nullptr;
   // state
   std::vector<Seq> seqs;
-  bool prefilled = false, poisoned = false;
+  bool prefilled = false;
+  std::atomic<bool> poisoned{false};   // also set by lane workers
   int64_t rounds = 0;
   std::string err;
   float *logits_tap = nullptr;
@@ -169,12 +188,19 @@ namespace {
 
 // A failed HIP call leaves device work of the call half done: the context
 // is poisoned.
+// A lane worker's failures go to its own message (merged by the round).
+thread_local std::string *t_lane_err = nullptr;
+void hip_failed(dex_ctx *ctx, const char *expr, hipError_t e) {
+  const std::string msg = std::string(expr) + ": " + hipGetErrorString(e);
+  if (t_lane_err != nullptr) *t_lane_err = msg;
+  else ctx->err = msg;
+  ctx->poisoned = true;
+}
 #define HIPCHK(expr)                                                          \
   do {                                                                        \
     hipError_t e_ = (expr);                                                   \
     if (e_ != hipSuccess) {                                                   \
-      ctx->err = std::string(#expr) + ": " + hipGetErrorString(e_);           \
-      ctx->poisoned = true;                                                   \
+      hip_failed(ctx, #expr, e_);                                             \
       return DEX_E_HIP;                                                       \
     }                                                                         \
   } while (0)
@@ -659,6 +685,45 @@ hipError_t scratch_address(void **out) {
   return hipSuccess;
 }
 
+// A lane worker: waits for a round (spinning for half a millisecond, then
+// sleeping in 2 ms slices), enqueues its lane's stages, reports.
+void lane_worker(dex_ctx *ctx, int lane) {
+  (void)hipSetDevice(ctx->device);
+  int64_t seen = 0;
+  for (;;) {
+    const auto t0 = std::chrono::steady_clock::now();
+    int64_t t;
+    while ((t = ctx->lane_ticket.load(std::memory_order_acquire)) == seen) {
+      if (ctx->lane_stop.load(std::memory_order_acquire)) return;
+      if (std::chrono::steady_clock::now() - t0 < std::chrono::microseconds(500)) continue;
+      std::unique_lock<std::mutex> lk(ctx->lane_mu);
+      ctx->lane_cv.wait_for(lk, std::chrono::milliseconds(2), [&] {
+        return ctx->lane_ticket.load(std::memory_order_acquire) != seen ||
+               ctx->lane_stop.load(std::memory_order_acquire);
+      });
+    }
+    seen = t;
+    std::string err;
+    t_lane_err = &err;
+    const dex_status st = ctx->lane_fn(lane);
+    t_lane_err = nullptr;
+    ctx->lane_status[lane] = st;
+    ctx->lane_err[lane] = std::move(err);
+    ctx->lane_done[lane].store(t, std::memory_order_release);
+  }
+}
+
+void stop_lane_workers(dex_ctx *ctx) {
+  if (ctx->lane_threads.empty()) return;
+  {
+    std::lock_guard<std::mutex> lk(ctx->lane_mu);
+    ctx->lane_stop.store(true, std::memory_order_release);
+  }
+  ctx->lane_cv.notify_all();
+  for (auto &th : ctx->lane_threads) th.join();
+  ctx->lane_threads.clear();
+}
+
 }  // namespace
 
 // ===================================================================== ABI
@@ -671,6 +736,7 @@ const char *dex_last_error(const dex_ctx *ctx) {
 
 void dex_destroy(dex_ctx *ctx) {
   if (!ctx) return;
+  stop_lane_workers(ctx);
   if (ctx->stream) (void)hipStreamSynchronize(ctx->stream);
   else (void)hipDeviceSynchronize();
   for (void *p : ctx->allocs) (void)hipFree(p);
@@ -895,6 +961,22 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       g_create_error = std::string("stream creation failed: ") + hipGetErrorString(e);
       dex_destroy(ctx);
       return DEX_E_HIP;
+    }
+    // a layer's weights under 64 MB stream in well under the ~2.5 us x 6
+    // launches the host needs to issue the layer: those models' rounds are
+    // bound by the issuing thread, so each extra lane gets its own
+    const double layer_bytes = (double)ctx->es * ((double)ctx->d * (ctx->H + 2 * ctx->Hkv) * ctx->hd +
+                                                  (double)ctx->H * ctx->hd * ctx->d + 3.0 * ctx->d * ctx->F);
+    if (ctx->n_lanes > 1 && layer_bytes <= 64.0 * (1 << 20)) {
+      (void)hipGetDevice(&ctx->device);
+      ctx->lane_done.reset(new std::atomic<int64_t>[ctx->n_lanes]());
+      ctx->lane_status.assign(ctx->n_lanes, DEX_OK);
+      ctx->lane_err.assign(ctx->n_lanes, std::string());
+      try {
+        for (int i = 1; i < ctx->n_lanes; ++i) ctx->lane_threads.emplace_back(lane_worker, ctx, i);
+      } catch (...) {
+        stop_lane_workers(ctx);       // fewer threads: the calling thread issues every lane
+      }
     }
   }
   ctx->seqs.resize(ctx->B);
@@ -1240,15 +1322,25 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     HIPCHK(hipEventRecord(ctx->fork_ev, ctx->stream));
     for (int i = 1; i < ctx->n_lanes; ++i) HIPCHK(hipStreamWaitEvent(ctx->lane_st[i], ctx->fork_ev, 0));
   }
-  int layers_streamed = 0, row_layers = 0, lane_next = 0;
-  double attn_bytes = 0.0;
-  for (int k = 0; k < N; ++k) {
+  // stages with rows go round-robin over the lanes
+  std::vector<int> stage_lane(N, -1);
+  {
+    int lane_next = 0;
+    for (int k = 0; k < N; ++k)
+      if (stage_r0[k + 1] > stage_r0[k]) stage_lane[k] = multi ? lane_next++ % ctx->n_lanes : 0;
+  }
+  struct LaneSum {
+    int layers = 0, row_layers = 0;
+    double attn_bytes = 0.0;
+  };
+  std::vector<LaneSum> lane_sum(ctx->n_lanes);
+  auto run_stage = [&](int k) -> dex_status {
     const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
-    if (M == 0) continue;
-    const hipStream_t lst = multi ? ctx->lane_st[lane_next++ % ctx->n_lanes] : ctx->stream;
+    const hipStream_t lst = multi ? ctx->lane_st[stage_lane[k]] : ctx->stream;
+    LaneSum &acc = lane_sum[stage_lane[k]];
     const std::vector<int> &ls = ctx->stage_layers[k];
-    layers_streamed += (int)ls.size();
-    row_layers += M * (int)ls.size();
+    acc.layers += (int)ls.size();
+    acc.row_layers += M * (int)ls.size();
     StageTables t{};
     t.seq = dptr(t_seq) + r0; t.pos = dptr(t_pos) + r0; t.entry = dptr(t_entry) + r0; t.bnd = dptr(t_bnd) + r0;
     t.tok = dptr(t_tok) + r0; t.nc = dptr(t_nc) + r0; t.chain_off = dptr(t_coff) + r0; t.chain = dptr(t_chain);
@@ -1264,8 +1356,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     }
     t.n_splits = std::min(ctx->jmax, stage_maxpos / ATT_SPLIT + 1);
     t.attn_bytes += (double)M * ctx->H * ctx->hd * (4.0 + ctx->es);
-
-    attn_bytes += t.attn_bytes * (double)ls.size();
+    acc.attn_bytes += t.attn_bytes * (double)ls.size();
     {
       PrepArgs p{};
       p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
@@ -1276,15 +1367,55 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
       TimedLaunch tl(ctx, 7, 0.0);
       HIPCHK(launch_prep(ctx->dtype, p, lst));
     }
-    dex_status rs = run_layers(ctx, lst, ls.front(), ls.back(), M, t, ctx->h_w + (size_t)r0 * ctx->d,
-                               ctx->part_w + (size_t)r0 * ctx->n_part,
-                               (char *)ctx->xb_w + (size_t)r0 * ctx->d * ctx->es,
-                               ctx->q_w + (size_t)r0 * ctx->H * ctx->hd,
-                               (char *)ctx->att_w + (size_t)r0 * ctx->H * ctx->hd * ctx->es,
-                               (char *)ctx->act_w + (size_t)r0 * ctx->F * ctx->es,
-                               ctx->attn_part + (size_t)r0 * ctx->H * ctx->jmax * (ctx->hd + 2), ctx->jmax,
-                               true, t.bnd);
+    return run_layers(ctx, lst, ls.front(), ls.back(), M, t, ctx->h_w + (size_t)r0 * ctx->d,
+                      ctx->part_w + (size_t)r0 * ctx->n_part,
+                      (char *)ctx->xb_w + (size_t)r0 * ctx->d * ctx->es,
+                      ctx->q_w + (size_t)r0 * ctx->H * ctx->hd,
+                      (char *)ctx->att_w + (size_t)r0 * ctx->H * ctx->hd * ctx->es,
+                      (char *)ctx->act_w + (size_t)r0 * ctx->F * ctx->es,
+                      ctx->attn_part + (size_t)r0 * ctx->H * ctx->jmax * (ctx->hd + 2), ctx->jmax,
+                      true, t.bnd);
+  };
+  if (multi && !ctx->lane_threads.empty()) {
+    // each lane's stages from its own thread (lane 0: this one), in stage order
+    auto run_lane = [&](int lane) -> dex_status {
+      for (int k = 0; k < N; ++k)
+        if (stage_lane[k] == lane) {
+          const dex_status st = run_stage(k);
+          if (st != DEX_OK) return st;
+        }
+      return DEX_OK;
+    };
+    ctx->lane_fn = run_lane;
+    const int64_t ticket = ctx->lane_ticket.load(std::memory_order_relaxed) + 1;
+    {
+      std::lock_guard<std::mutex> lk(ctx->lane_mu);
+      ctx->lane_ticket.store(ticket, std::memory_order_release);
+    }
+    ctx->lane_cv.notify_all();
+    dex_status rs = run_lane(0);
+    for (int i = 1; i < ctx->n_lanes; ++i) {
+      while (ctx->lane_done[i].load(std::memory_order_acquire) != ticket) std::this_thread::yield();
+      if (rs == DEX_OK && ctx->lane_status[i] != DEX_OK) {
+        rs = ctx->lane_status[i];
+        ctx->err = ctx->lane_err[i];
+      }
+    }
+    ctx->lane_fn = nullptr;
     if (rs != DEX_OK) return fail(ctx, rs);
+  } else {
+    for (int k = 0; k < N; ++k) {
+      if (stage_lane[k] < 0) continue;
+      const dex_status rs = run_stage(k);
+      if (rs != DEX_OK) return fail(ctx, rs);
+    }
+  }
+  int layers_streamed = 0, row_layers = 0;
+  double attn_bytes = 0.0;
+  for (const LaneSum &ls : lane_sum) {
+    layers_streamed += ls.layers;
+    row_layers += ls.row_layers;
+    attn_bytes += ls.attn_bytes;
   }
   if (multi) {
     for (int i = 1; i < ctx->n_lanes; ++i) {
