@@ -115,9 +115,8 @@ struct dex_ctx {
   std::vector<hipStream_t> lane_st;
   std::vector<hipEvent_t> lane_ev;
   hipEvent_t fork_ev = nullptr;
-  // lane workers, for models whose kernels take about as long as the host
-  // takes to issue a launch (~2.5 us): lanes 1.. enqueue their stages from
-  // host threads of their own while the calling thread enqueues lane 0's
+  // lane workers: lanes 1.. enqueue their stages from host threads of their
+  // own while the calling thread enqueues lane 0's
   int device = 0;
   std::vector<std::thread> lane_threads;
   std::atomic<int64_t> lane_ticket{0};           // round handed to the workers
@@ -962,12 +961,11 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
       dex_destroy(ctx);
       return DEX_E_HIP;
     }
-    // a layer's weights under 64 MB stream in well under the ~2.5 us x 6
-    // launches the host needs to issue the layer: those models' rounds are
-    // bound by the issuing thread, so each extra lane gets its own
-    const double layer_bytes = (double)ctx->es * ((double)ctx->d * (ctx->H + 2 * ctx->Hkv) * ctx->hd +
-                                                  (double)ctx->H * ctx->hd * ctx->d + 3.0 * ctx->d * ctx->F);
-    if (ctx->n_lanes > 1 && layer_bytes <= 64.0 * (1 << 20)) {
+    // each extra lane issues its stages from a host thread of its own: the
+    // host needs ~2.5 us per launch, which bounds the rounds of models with
+    // short kernels, and issuing the lanes one after another also staggers
+    // their starts on larger models
+    if (ctx->n_lanes > 1) {
       (void)hipGetDevice(&ctx->device);
       ctx->lane_done.reset(new std::atomic<int64_t>[ctx->n_lanes]());
       ctx->lane_status.assign(ctx->n_lanes, DEX_OK);
