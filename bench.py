@@ -59,6 +59,10 @@ def parse():
     p.add_argument("--temperature", type=float, default=0.0,
                    help="> 0: Algorithm 2's sampling mode (Gumbel-max, seed --seed); 0: greedy")
     p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--stage-grouping", type=int, default=0, choices=(0, 1, -1),
+                   help="0/1: each lane's stages in step, one launch per kernel and layer step; "
+                        "-1: launches per stage")
+    p.add_argument("--stage-streams", type=int, default=0, help="lanes (0: the library default)")
     p.add_argument("--adapter-alpha", type=float, default=None,
                    help="attach synthetic inducing adapters with this gate to the non-final depths")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
@@ -142,7 +146,8 @@ def main():
     if need > cfg["gen_len"]:
         max_ctx = P + need
 
-    samp = dict(temperature=args.temperature, seed=args.seed)
+    samp = dict(temperature=args.temperature, seed=args.seed, stage_grouping=args.stage_grouping,
+                stage_streams=args.stage_streams)
     dev_ad = None
     if args.adapter_alpha is not None:
         dev_ad = dexlib.device_weights(cfg, gen.generate_adapters(cfg, args.adapter_alpha))
@@ -364,6 +369,7 @@ def main():
         "data": "synthetic (seeded random weights and uniform prompts)",
         "config": {"workload": cfg["name"], "explored": cfg["explored"], "width_cap": cfg["width_cap"],
                    "batch": B, "prompt_len": P, "parallelism": "single GPU",
+                   "stage_launches": "grouped" if args.stage_grouping >= 0 else "per stage",
                    "decoding": (f"sampling, temperature {args.temperature}, seed {args.seed}"
                                 if args.temperature > 0 else "greedy"),
                    "adapters": (f"synthetic, gate {args.adapter_alpha}" if args.adapter_alpha is not None

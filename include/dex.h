@@ -120,10 +120,11 @@ typedef struct {
   int32_t batch;                        /* independent sequences, 1 .. DEX_MAX_BATCH */
   int32_t max_context;                  /* prompt length + generated tokens, per sequence */
   void *hip_stream;                     /* hipStream_t or NULL */
-  int32_t stage_streams;                /* streams a round's stages are spread over: the
-                                           stages of one round read and write disjoint
-                                           state, so they may run concurrently.  0: the
-                                           library default; 1: everything on hip_stream */
+  int32_t stage_streams;                /* streams (lanes) a round's stages are spread
+                                           over: the stages of one round read and write
+                                           disjoint state, so they may run concurrently.
+                                           0: the library default; 1: everything on
+                                           hip_stream */
   float temperature;                    /* 0: greedy decoding.  > 0: Algorithm 2's sampling
                                            mode, every node decodes argmax(l / temperature
                                            + G) with G the Gumbel row of (sample_seed,
@@ -140,6 +141,13 @@ typedef struct {
                                            W2 [d][m], b2 float[d], alpha float[1]; matrices in
                                            weight_dtype.  Borrowed: read at create (the
                                            library keeps repacked copies and alpha) */
+  int32_t stage_grouping;               /* 0 (default) or 1: each lane takes a contiguous run
+                                           of the round's stages and runs them in step, each
+                                           kernel launched once per layer step for every
+                                           stage of the run that has that step; -1: each
+                                           stage's layers launched on their own, the stages
+                                           dealt round-robin over the lanes.  The results
+                                           are the same bits either way. */
 } dex_config;
 
 /* What one dex_step did (all host memory).  Rows are listed stage-major,

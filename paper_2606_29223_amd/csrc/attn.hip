@@ -595,6 +595,42 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   attn_mfma_item<HD>(a, blockIdx.x, blockIdx.y, vr, prow, ppos);
 }
 
+// The arguments of segment sg alone: its layer of the cache, its queries,
+// rows and row groups, and the split records of its rows in the launch's
+// row space (records of element type T).
+template <typename T>
+static __host__ __device__ inline void attn_seg_view(AttnArgs &a, const AttnSeg &sg) {
+  const size_t r0 = (size_t)sg.r0;
+  a.kc = sg.kc;
+  a.vc = sg.vc;
+  a.q += r0 * a.ldq;
+  a.row_pos += r0;
+  a.row_nc += r0;
+  a.row_chain_off += r0;
+  a.row_seq += r0;
+  a.grp_row0 += sg.g0;
+  a.grp_nrows += sg.g0;
+  a.grp_seq += sg.g0;
+  a.n_rows = sg.M;
+  a.n_splits = sg.n_splits;
+  a.part = (T *)a.part + r0 * a.n_heads * a.jmax * a.head_dim;
+  a.stat += r0 * a.n_heads * a.jmax * 2;
+}
+
+// Grouped form: block x runs item x - item0 of the segment whose items hold it.
+template <int HD>
+__global__ __launch_bounds__(64) void attn_mfma_seg_kernel(AttnArgs a, AttnSegs g) {
+  __shared__ __attribute__((aligned(16))) uint16_t vr[ATT_SPLIT][HD + 16];
+  __shared__ int prow[ATT_MAX_PAIRS];
+  __shared__ int ppos[ATT_MAX_PAIRS];
+  const int x = blockIdx.x;
+  int k = 0;
+#pragma unroll
+  for (int i = 1; i < MAX_SEGS; ++i) k += (i < g.n && x >= g.item0[i]) ? 1 : 0;
+  attn_seg_view<bf16>(a, g.s[k]);
+  attn_mfma_item<HD>(a, x - g.item0[k], blockIdx.y, vr, prow, ppos);
+}
+
 // Causal prompt attention for head_dim 128 (bf16), G query heads per kv
 // head with G in {1, 2, 4, 8}.  Workgroup = (32 query rows, kv head,
 // sequence), wave w = query head kvh * G + w; blocks of 64 keys stream into
@@ -816,6 +852,55 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStrea
     return hipGetLastError();
   }
   return dtype == 1 ? launch_attn_t<bf16>(a, grid, s) : launch_attn_t<float>(a, grid, s);
+}
+
+// The matrix-core kernel: up to MAX_SEGS segments per launch, a lone segment
+// as a plain launch; the other kernels: one launch per segment.
+hipError_t launch_attention_seg(int dtype, const AttnArgs &a, const AttnSeg *segs, int n, hipStream_t s) {
+  if (segs == nullptr || n < 1 || a.n_heads / a.n_kv_heads > 8) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i) {
+    const AttnSeg &sg = segs[i];
+    if (sg.M < 1 || sg.r0 < 0 || sg.g0 < 0 || sg.n_groups < 1 || sg.n_splits < 1 || sg.n_splits > a.jmax)
+      return hipErrorInvalidValue;
+  }
+  if (!(dtype == 1 && (a.head_dim == 128 || a.head_dim == 64))) {
+    for (int i = 0; i < n; ++i) {
+      AttnArgs b = a;
+      if (dtype == 1) attn_seg_view<bf16>(b, segs[i]);
+      else attn_seg_view<float>(b, segs[i]);
+      const hipError_t e = launch_attention(dtype, b, segs[i].n_groups, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  if (a.row_seq == nullptr) return hipErrorInvalidValue;
+  for (int i0 = 0; i0 < n; i0 += MAX_SEGS) {
+    const int c = n - i0 < MAX_SEGS ? n - i0 : MAX_SEGS;
+    if (c == 1) {
+      AttnArgs b = a;
+      attn_seg_view<bf16>(b, segs[i0]);
+      const hipError_t e = launch_attention(1, b, segs[i0].n_groups, s);
+      if (e != hipSuccess) return e;
+      continue;
+    }
+    AttnSegs g{};
+    g.n = c;
+    size_t items = 0;
+    for (int i = 0; i < c; ++i) {
+      const AttnSeg &sg = segs[i0 + i];
+      g.s[i] = sg;
+      g.item0[i] = (int)items;
+      items += 2 * (size_t)sg.M + (size_t)sg.n_groups * sg.n_splits;
+      if (items > 0x7fffffffull) return hipErrorInvalidValue;
+    }
+    for (int i = c; i < MAX_SEGS; ++i) g.item0[i] = (int)items;
+    const dim3 grid((unsigned)items, a.n_kv_heads);
+    if (a.head_dim == 128) hipLaunchKernelGGL(attn_mfma_seg_kernel<128>, grid, dim3(64), 0, s, a, g);
+    else hipLaunchKernelGGL(attn_mfma_seg_kernel<64>, grid, dim3(64), 0, s, a, g);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace dex

@@ -153,6 +153,72 @@ struct CombineArgs {
   int ld_out;
 };
 
+// Grouped launches.  The stages of a round are independent and, taken in
+// step, all run their j-th layer at the same time: one launch then covers
+// that layer step of every stage (a segment each), each segment on its own
+// rows of the launch's row space with its own layer's weights and cache.  A
+// segment's rows go through exactly the arithmetic of a launch of their own
+// (segments never share a workgroup), so grouping changes no result bit.
+// A launch takes at most MAX_SEGS segments in its arguments (longer lists go
+// out as several launches), and a single segment goes out as a plain launch
+// of the same rows: the arguments stay small, which keeps the launch cost of
+// short kernels down.
+constexpr int MAX_SEGS = 8;
+
+struct GemmSeg {
+  const void *wp;             // the segment's layer weights (packed)
+  void *kc, *vc;              // QKV: the layer's key/value cache base
+  const float *g_next;        // RESID: the next RMSNorm's gain (nullptr: none)
+  const int *row_bnd;         // RESID: boundary rows of the segment (nullable)
+  float alpha;                // RESID: the layer's residual scale
+  int r0, M;                  // rows [r0, r0 + M) of the launch's buffers
+};
+struct GemmSegs {
+  int n;
+  GemmSeg s[MAX_SEGS];
+};
+
+// The arguments of segment s alone: its weights and layer, and the
+// row-indexed buffers and tables advanced to its first row.
+template <typename T, int EPI>
+__host__ __device__ inline void gemm_seg_view(GemmArgs &a, const GemmSeg &s) {
+  static_assert(EPI == EPI_QKV || EPI == EPI_RESID || EPI == EPI_SWIGLU, "grouped epilogues");
+  const size_t r = (size_t)s.r0;
+  a.wp = s.wp;
+  a.M = s.M;
+  a.x = (const T *)a.x + r * a.ldx;
+  if (a.part != nullptr) a.part += r * a.n_part;
+  if constexpr (EPI == EPI_QKV) {
+    a.out += r * a.ld_out;
+    a.kc = s.kc;
+    a.vc = s.vc;
+    a.row_seq += r;
+    a.row_pos += r;
+    a.row_entry += r;
+  } else if constexpr (EPI == EPI_RESID) {
+    a.h += r * a.ld_h;
+    a.alpha = s.alpha;
+    a.g_next = s.g_next;
+    a.xb = s.g_next != nullptr ? (void *)((T *)a.xb + r * a.ld_h) : nullptr;
+    a.part_out += r * a.n_part_out;
+    a.row_bnd = s.row_bnd;
+  } else {
+    a.act = (T *)a.act + r * a.ld_act;
+  }
+}
+
+struct AttnSeg {
+  const void *kc, *vc;        // the segment's layer of the cache
+  int r0, M;                  // its rows [r0, r0 + M) of the queries and row tables
+  int g0, n_groups;           // its row groups [g0, g0 + n_groups) (row0 relative to r0)
+  int n_splits;               // 64-key splits up to its deepest row
+};
+struct AttnSegs {
+  int n;
+  int item0[MAX_SEGS];        // first work item of each segment (set by the launcher)
+  AttnSeg s[MAX_SEGS];
+};
+
 // Causal prompt attention on the matrix cores (bf16 keys/values, head_dim 64
 // or 128): rows are (sequence, position) in order, keys are the committed
 // cache entries 0..position.
@@ -194,6 +260,13 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs &a, hipStream_t s);
 hipError_t launch_row_scale(const float *part, int n_part, int M, float inv_d, float eps, float *out, hipStream_t s);
 hipError_t launch_attention(int dtype, const AttnArgs &a, int n_groups, hipStream_t s);
 hipError_t launch_combine(int dtype, const CombineArgs &a, int rows, hipStream_t s);
+// Grouped forms (QKV, RESID and SWIGLU epilogues; the decode attention):
+// `a` holds what the segments share, with the row-indexed buffers and tables
+// at row 0 of the launch.  The attention's split records then use the row
+// space of the launch: part [rows][H][jmax][hd], stat at split_stats(part,
+// rows, ...), where rows covers every segment.
+hipError_t launch_gemm_seg(int dtype, int epi, const GemmArgs &a, const GemmSeg *segs, int n, hipStream_t s);
+hipError_t launch_attention_seg(int dtype, const AttnArgs &a, const AttnSeg *segs, int n, hipStream_t s);
 
 struct PrepArgs {
   int M, d, n_part;

@@ -37,8 +37,15 @@ using namespace dex;
 
 namespace {
 
-// streams a round's stages are spread over unless the caller says otherwise
+// streams a round's stages are spread over unless the caller says otherwise:
+// launched per stage, four; grouped, three where a layer's weights take long
+// enough to stream that another lane's latency-bound attention and combine
+// hide behind them, else one (models whose kernels are bound by launch costs
+// gain most from the fewest launches: measured on the 32-layer d4096 and the
+// 12-layer d768 models)
 constexpr int kDefaultStageStreams = 4;
+constexpr int kDefaultGroupedStreams = 3;
+constexpr double kLaneLayerBytes = 64e6;
 
 // round phases reported by dex_debug_round_times
 constexpr int kRoundPhases = 7;
@@ -112,6 +119,9 @@ struct dex_ctx {
   // the caller's stream as a lane measured ~10 % faster than four library
   // streams: fewer streams than the process's hardware queues to share)
   int n_lanes = 1;
+  // grouped launches: the stages of a lane run in step, one launch per
+  // kernel and layer step for all of them
+  bool grouped = false;
   std::vector<hipStream_t> lane_st;
   std::vector<hipEvent_t> lane_ev;
   hipEvent_t fork_ev = nullptr;
@@ -943,7 +953,12 @@ dex_status dex_create(const dex_model *m, const dex_config *c, dex_ctx **out) {
   }
   // stage lanes (default priority, non-blocking streams)
   {
-    ctx->n_lanes = c->stage_streams > 0 ? std::min<int>(c->stage_streams, 8) : kDefaultStageStreams;
+    ctx->grouped = c->stage_grouping >= 0;
+    const double layer_bytes = (double)ctx->es * ((double)ctx->d * (ctx->H + 2 * ctx->Hkv) * ctx->hd +
+                                                   (double)ctx->H * ctx->hd * ctx->d + 3.0 * ctx->d * ctx->F);
+    const int def_lanes = !ctx->grouped ? kDefaultStageStreams
+                          : layer_bytes >= kLaneLayerBytes ? kDefaultGroupedStreams : 1;
+    ctx->n_lanes = c->stage_streams > 0 ? std::min<int>(c->stage_streams, 8) : def_lanes;
     ctx->lane_st.assign(ctx->n_lanes, ctx->stream);
     ctx->lane_ev.assign(ctx->n_lanes, nullptr);
     hipError_t e = hipSuccess;
@@ -1321,8 +1336,16 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     for (int i = 1; i < ctx->n_lanes; ++i) HIPCHK(hipStreamWaitEvent(ctx->lane_st[i], ctx->fork_ev, 0));
   }
   // stages with rows go round-robin over the lanes
+  // (grouped: contiguous runs of them, one per lane, so that each lane's rows
+  // are consecutive)
   std::vector<int> stage_lane(N, -1);
-  {
+  if (ctx->grouped) {
+    std::vector<int> act;
+    for (int k = 0; k < N; ++k)
+      if (stage_r0[k + 1] > stage_r0[k]) act.push_back(k);
+    const int na = (int)act.size(), nl = multi ? std::min(ctx->n_lanes, na) : 1;
+    for (int i = 0; i < na; ++i) stage_lane[act[i]] = i * nl / na;
+  } else {
     int lane_next = 0;
     for (int k = 0; k < N; ++k)
       if (stage_r0[k + 1] > stage_r0[k]) stage_lane[k] = multi ? lane_next++ % ctx->n_lanes : 0;
@@ -1332,14 +1355,16 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     double attn_bytes = 0.0;
   };
   std::vector<LaneSum> lane_sum(ctx->n_lanes);
-  auto run_stage = [&](int k) -> dex_status {
+  // a stage's tables, its share of the round's sums, and the launch that
+  // gives its rows their first RMSNorm input (from the embedding or the
+  // boundary state their slot reached)
+  auto stage_prologue = [&](int k, StageTables &t, hipStream_t lst) -> dex_status {
     const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
-    const hipStream_t lst = multi ? ctx->lane_st[stage_lane[k]] : ctx->stream;
     LaneSum &acc = lane_sum[stage_lane[k]];
     const std::vector<int> &ls = ctx->stage_layers[k];
     acc.layers += (int)ls.size();
     acc.row_layers += M * (int)ls.size();
-    StageTables t{};
+    t = StageTables{};
     t.seq = dptr(t_seq) + r0; t.pos = dptr(t_pos) + r0; t.entry = dptr(t_entry) + r0; t.bnd = dptr(t_bnd) + r0;
     t.tok = dptr(t_tok) + r0; t.nc = dptr(t_nc) + r0; t.chain_off = dptr(t_coff) + r0; t.chain = dptr(t_chain);
     t.g_row0 = dptr(t_g0) + stage_g0[k]; t.g_nrows = dptr(t_gn) + stage_g0[k]; t.g_seq = dptr(t_gs) + stage_g0[k];
@@ -1365,6 +1390,15 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
       TimedLaunch tl(ctx, 7, 0.0);
       HIPCHK(launch_prep(ctx->dtype, p, lst));
     }
+    return DEX_OK;
+  };
+  auto run_stage = [&](int k) -> dex_status {
+    const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
+    const hipStream_t lst = multi ? ctx->lane_st[stage_lane[k]] : ctx->stream;
+    const std::vector<int> &ls = ctx->stage_layers[k];
+    StageTables t{};
+    const dex_status ps = stage_prologue(k, t, lst);
+    if (ps != DEX_OK) return ps;
     return run_layers(ctx, lst, ls.front(), ls.back(), M, t, ctx->h_w + (size_t)r0 * ctx->d,
                       ctx->part_w + (size_t)r0 * ctx->n_part,
                       (char *)ctx->xb_w + (size_t)r0 * ctx->d * ctx->es,
@@ -1374,16 +1408,184 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
                       ctx->attn_part + (size_t)r0 * ctx->H * ctx->jmax * (ctx->hd + 2), ctx->jmax,
                       true, t.bnd);
   };
-  if (multi && !ctx->lane_threads.empty()) {
-    // each lane's stages from its own thread (lane 0: this one), in stage order
-    auto run_lane = [&](int lane) -> dex_status {
-      for (int k = 0; k < N; ++k)
-        if (stage_lane[k] == lane) {
-          const dex_status st = run_stage(k);
-          if (st != DEX_OK) return st;
+  // grouped: a lane's stages in step, layer step j of every one of them that
+  // has one in a single launch per kernel (segments in stage order, whose
+  // rows are consecutive in the round's buffers)
+  auto run_grouped = [&](int lane) -> dex_status {
+    const int d = ctx->d, H = ctx->H, Hkv = ctx->Hkv, hd = ctx->hd, F = ctx->F, jmax = ctx->jmax;
+    const size_t layer_kv = (size_t)B * Hkv * ctx->E * hd * ctx->es;
+    const hipStream_t st = multi ? ctx->lane_st[lane] : ctx->stream;
+    std::vector<int> ks;
+    std::vector<StageTables> tabs(N);
+    size_t depth = 0;
+    for (int k = 0; k < N; ++k) {
+      if (stage_lane[k] != lane) continue;
+      const dex_status ps = stage_prologue(k, tabs[k], st);
+      if (ps != DEX_OK) return ps;
+      ks.push_back(k);
+      depth = std::max(depth, ctx->stage_layers[k].size());
+    }
+    // split records of every row of the round: [R][H][jmax][hd], then the
+    // statistics
+    float *stat_all = split_stats(ctx->attn_part, R, H, jmax, hd);
+    const size_t rec_row = (size_t)H * jmax * hd * ctx->es;     // record bytes per row
+    std::vector<int> on, lay;
+    std::vector<GemmSeg> gs(ks.size());
+    std::vector<AttnSeg> as(ks.size());
+    for (size_t j = 0; j < depth; ++j) {
+      on.clear();
+      lay.clear();
+      for (int k : ks)
+        if (j < ctx->stage_layers[k].size()) {
+          on.push_back(k);
+          lay.push_back(ctx->stage_layers[k][j]);
         }
-      return DEX_OK;
-    };
+      const int n = (int)on.size();
+      auto seg_rows = [&](GemmSeg &g, int i) {
+        g.r0 = stage_r0[on[i]];
+        g.M = stage_r0[on[i] + 1] - g.r0;
+      };
+      // QKV
+      {
+        GemmArgs a{};
+        a.nsteps_w = ctx->ns_d; a.N = (H + 2 * Hkv) * hd; a.K = d;
+        a.x = ctx->xb_w; a.ldx = d;
+        a.part = ctx->part_w; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+        a.out = ctx->q_w; a.ld_out = H * hd;
+        a.kv_entries = ctx->E; a.n_heads = H; a.n_kv_heads = Hkv; a.head_dim = hd;
+        a.row_seq = dptr(t_seq); a.row_pos = dptr(t_pos); a.row_entry = dptr(t_entry); a.rope = ctx->rope;
+        double bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+          const int l = lay[i];
+          GemmSeg &g = gs[i];
+          g = GemmSeg{};
+          g.wp = ctx->p_qkv[l];
+          g.kc = (char *)ctx->kc + l * layer_kv;
+          g.vc = (char *)ctx->vc + l * layer_kv;
+          seg_rows(g, i);
+          bytes += wbytes(ctx, (double)a.N * d + (double)g.M * d + 2.0 * g.M * Hkv * hd) + 4.0 * g.M * H * hd;
+        }
+        TimedLaunch tl(ctx, 0, bytes);
+        HIPCHK(launch_gemm_seg(ctx->dtype, EPI_QKV, a, gs.data(), n, st));
+      }
+      // attention
+      {
+        AttnArgs a{};
+        a.q = ctx->q_w; a.ldq = H * hd;
+        a.kv_entries = ctx->E; a.n_kv_heads = Hkv; a.n_heads = H; a.head_dim = hd; a.batch = B;
+        a.grp_row0 = dptr(t_g0); a.grp_nrows = dptr(t_gn); a.grp_seq = dptr(t_gs);
+        a.row_pos = dptr(t_pos); a.row_nc = dptr(t_nc); a.row_chain_off = dptr(t_coff); a.chain = dptr(t_chain);
+        a.row_seq = dptr(t_seq);
+        a.part = ctx->attn_part; a.stat = stat_all;
+        a.jmax = jmax; a.scale = 1.0f / std::sqrt((float)hd);
+        double bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+          const int k = on[i], l = lay[i];
+          AttnSeg &g = as[i];
+          g.kc = (char *)ctx->kc + l * layer_kv;
+          g.vc = (char *)ctx->vc + l * layer_kv;
+          g.r0 = stage_r0[k];
+          g.M = stage_r0[k + 1] - stage_r0[k];
+          g.g0 = stage_g0[k];
+          g.n_groups = tabs[k].n_groups;
+          g.n_splits = tabs[k].n_splits;
+          bytes += tabs[k].attn_bytes;
+        }
+        TimedLaunch tl(ctx, 1, bytes);
+        HIPCHK(launch_attention_seg(ctx->dtype, a, as.data(), n, st));
+      }
+      // split combine over each run of consecutive rows
+      for (int i = 0; i < n;) {
+        const int ra = stage_r0[on[i]];
+        int rb = stage_r0[on[i] + 1], e = i + 1;
+        while (e < n && stage_r0[on[e]] == rb) rb = stage_r0[on[e++] + 1];
+        CombineArgs c{};
+        c.part = (char *)ctx->attn_part + ra * rec_row;
+        c.stat = stat_all + (size_t)ra * H * jmax * 2;
+        c.row_pos = dptr(t_pos) + ra; c.jmax = jmax; c.n_heads = H; c.head_dim = hd;
+        c.out = (char *)ctx->att_w + (size_t)ra * H * hd * ctx->es; c.ld_out = H * hd;
+        TimedLaunch tl(ctx, 2, 0.0);
+        HIPCHK(launch_combine(ctx->dtype, c, rb - ra, st));
+        i = e;
+      }
+      // O projection + residual
+      {
+        GemmArgs a{};
+        a.nsteps_w = ctx->ns_hhd; a.N = d; a.K = H * hd;
+        a.x = ctx->att_w; a.ldx = H * hd;
+        a.h = ctx->h_w; a.ld_h = d; a.xb = ctx->xb_w;
+        a.part_out = ctx->part_w; a.n_part_out = ctx->n_part;
+        double bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+          const int l = lay[i];
+          GemmSeg &g = gs[i];
+          g = GemmSeg{};
+          g.wp = ctx->p_o[l];
+          g.alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
+          g.g_next = (const float *)LW(ctx, l, DEX_P_FFN_NORM);
+          seg_rows(g, i);
+          bytes += wbytes(ctx, (double)d * H * hd + (double)g.M * H * hd + (double)g.M * d) + 8.0 * g.M * d;
+        }
+        TimedLaunch tl(ctx, 3, bytes);
+        HIPCHK(launch_gemm_seg(ctx->dtype, EPI_RESID, a, gs.data(), n, st));
+      }
+      // gate/up + SiLU
+      {
+        GemmArgs a{};
+        a.nsteps_w = ctx->ns_d; a.N = F; a.K = d;
+        a.x = ctx->xb_w; a.ldx = d;
+        a.part = ctx->part_w; a.n_part = ctx->n_part; a.inv_d = 1.0f / d; a.eps = ctx->eps;
+        a.act = ctx->act_w; a.ld_act = F;
+        double bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+          GemmSeg &g = gs[i];
+          g = GemmSeg{};
+          g.wp = ctx->p_gu[lay[i]];
+          seg_rows(g, i);
+          bytes += wbytes(ctx, 2.0 * F * d + (double)g.M * d + (double)g.M * F);
+        }
+        TimedLaunch tl(ctx, 4, bytes);
+        HIPCHK(launch_gemm_seg(ctx->dtype, EPI_SWIGLU, a, gs.data(), n, st));
+      }
+      // down + residual; a stage's last layer writes its rows' boundary state
+      {
+        GemmArgs a{};
+        a.nsteps_w = ctx->ns_F; a.N = d; a.K = F;
+        a.x = ctx->act_w; a.ldx = F;
+        a.h = ctx->h_w; a.ld_h = d; a.xb = ctx->xb_w;
+        a.part_out = ctx->part_w; a.n_part_out = ctx->n_part;
+        a.bnd_h = ctx->bnd_h; a.bnd_part = ctx->bnd_part;
+        double bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+          const int k = on[i], l = lay[i];
+          const bool last = (j + 1 == ctx->stage_layers[k].size());
+          GemmSeg &g = gs[i];
+          g = GemmSeg{};
+          g.wp = ctx->p_down[l];
+          g.alpha = ctx->rscale * (float)(l + 1) / (float)ctx->L;
+          g.g_next = last ? nullptr : (const float *)LW(ctx, l + 1, DEX_P_ATTN_NORM);
+          g.row_bnd = last ? tabs[k].bnd : nullptr;
+          seg_rows(g, i);
+          bytes += wbytes(ctx, (double)d * F + (double)g.M * F + (double)g.M * d) + 8.0 * g.M * d;
+        }
+        TimedLaunch tl(ctx, 5, bytes);
+        HIPCHK(launch_gemm_seg(ctx->dtype, EPI_RESID, a, gs.data(), n, st));
+      }
+    }
+    return DEX_OK;
+  };
+  // a lane's stages, in stage order
+  auto run_lane = [&](int lane) -> dex_status {
+    if (ctx->grouped) return run_grouped(lane);
+    for (int k = 0; k < N; ++k)
+      if (stage_lane[k] == lane) {
+        const dex_status st = run_stage(k);
+        if (st != DEX_OK) return st;
+      }
+    return DEX_OK;
+  };
+  if (multi && !ctx->lane_threads.empty()) {
+    // each lane from its own thread (lane 0: this one)
     ctx->lane_fn = run_lane;
     const int64_t ticket = ctx->lane_ticket.load(std::memory_order_relaxed) + 1;
     {
@@ -1402,9 +1604,8 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     ctx->lane_fn = nullptr;
     if (rs != DEX_OK) return fail(ctx, rs);
   } else {
-    for (int k = 0; k < N; ++k) {
-      if (stage_lane[k] < 0) continue;
-      const dex_status rs = run_stage(k);
+    for (int lane = 0; lane < ctx->n_lanes; ++lane) {
+      const dex_status rs = run_lane(lane);
       if (rs != DEX_OK) return fail(ctx, rs);
     }
   }

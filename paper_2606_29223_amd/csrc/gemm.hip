@@ -36,7 +36,7 @@ namespace dex {
 // per weight byte.  A tile's sums are the same per-wave partials added in
 // the same order whatever NTW is, so neither changes any result bit.
 template <typename T, int EPI, int MB, int U, int NTW>
-__global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs &a) {
   using F = Frag<T>;
   constexpr int EPB = F::EPB;
   constexpr int KSTEP = 4 * EPB;               // k covered by one 16-byte step of a wave
@@ -249,6 +249,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
   }
 }
 
+template <typename T, int EPI, int MB, int U, int NTW>
+__global__ __launch_bounds__(GEMM_THREADS) void gemm_kernel(GemmArgs a) {
+  gemm_tile<T, EPI, MB, U, NTW>(a);
+}
+
+// Segment blockIdx.z of a grouped launch (gemm_seg_view); row blocks past
+// its rows have nothing to do.
+template <typename T, int EPI, int MB, int U, int NTW>
+__global__ __launch_bounds__(GEMM_THREADS) void gemm_seg_kernel(GemmArgs a, GemmSegs g) {
+  gemm_seg_view<T, EPI>(a, g.s[blockIdx.z]);
+  if ((int)blockIdx.y * 16 * MB >= a.M) return;
+  gemm_tile<T, EPI, MB, U, NTW>(a);
+}
+
 // Weight packing: block (tile, step, t) holds, for lane l, the 16 bytes of
 // row col(tile, l % 16) at k = step * KSTEP + (l / 16) * EPB (zeros beyond
 // N or K), so that a wave's load of one MFMA step is one contiguous 1 KB.
@@ -295,21 +309,34 @@ hipError_t launch_pack(int dtype, const PackArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// One launch of the chosen configuration: plain, or grouped over g's
+// segments (grid z).
+template <typename T, int EPI, int MB, int U, int NTW>
+static void go(const GemmArgs &a, const GemmSegs *g, dim3 grid, hipStream_t s) {
+  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID || EPI == EPI_SWIGLU) {
+    if (g != nullptr) {
+      hipLaunchKernelGGL((gemm_seg_kernel<T, EPI, MB, U, NTW>), dim3(grid.x, grid.y, g->n), dim3(GEMM_THREADS), 0,
+                         s, a, *g);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((gemm_kernel<T, EPI, MB, U, NTW>), grid, dim3(GEMM_THREADS), 0, s, a);
+}
+
+// The configuration for M rows (a grouped launch: its largest segment's).
 template <typename T, int EPI>
-static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
+static hipError_t launch_t(const GemmArgs &a, const GemmSegs *g, int M, hipStream_t s) {
   const int n_tiles = (a.N + 15) / 16;
-  dim3 block(GEMM_THREADS);
-  if (m_blocks <= 0) return hipErrorInvalidValue;
-  if (a.M <= 16) {
+  if (M <= 16) {
     // deeper prefetch when a workgroup per CU streams a long tile, shallower
     // when many workgroups share each CU (measured on the 4096-wide layers);
     // from 5 rows on, the wide matrices (gate/up, LM head) take two tiles per
     // workgroup so that each activation load feeds two weight tiles
-    if (a.M > 4 && n_tiles > 512)
-      hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2, 2>), dim3((n_tiles + 1) / 2, 1), block, 0, s, a);
-    else if (n_tiles <= 256) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
-    else if (n_tiles <= 1024) hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 2, 1>), dim3(n_tiles, 1), block, 0, s, a);
+    if (M > 4 && n_tiles > 512)
+      go<T, EPI, 1, 2, 2>(a, g, dim3((n_tiles + 1) / 2, 1), s);
+    else if (n_tiles <= 256) go<T, EPI, 1, 8, 1>(a, g, dim3(n_tiles, 1), s);
+    else if (n_tiles <= 1024) go<T, EPI, 1, 4, 1>(a, g, dim3(n_tiles, 1), s);
+    else go<T, EPI, 1, 2, 1>(a, g, dim3(n_tiles, 1), s);
   } else {
     // more rows: the wide matrices take several weight tiles per workgroup
     // so that each activation load feeds them all -- four for the 2000-tile
@@ -319,48 +346,94 @@ static hipError_t launch_t(const GemmArgs &a, int m_blocks, hipStream_t s) {
     // activation load feeding two tiles); the 384-tile QKV keeps one tile
     // per workgroup (measured per class at 17-64 rows); with 64-row blocks
     // the reduction buffer takes most of the LDS
-    if (a.M <= 32) {
+    if (M <= 32) {
       if constexpr (EPI == EPI_LOGITS || EPI == EPI_SWIGLU)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 2, 4>), dim3((n_tiles + 3) / 4, 1), block, 0, s, a);
-      else if (n_tiles <= 256 && a.M > 24)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, 8, 2>), dim3((n_tiles + 1) / 2, 2), block, 0, s, a);
+        go<T, EPI, 2, 2, 4>(a, g, dim3((n_tiles + 3) / 4, 1), s);
+      else if (n_tiles <= 256 && M > 24)
+        go<T, EPI, 1, 8, 2>(a, g, dim3((n_tiles + 1) / 2, 2), s);
       else if (n_tiles <= 256)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 8, 1>), dim3(n_tiles, 1), block, 0, s, a);
+        go<T, EPI, 2, 8, 1>(a, g, dim3(n_tiles, 1), s);
       else
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 1>), dim3(n_tiles, 1), block, 0, s, a);
+        go<T, EPI, 2, 4, 1>(a, g, dim3(n_tiles, 1), s);
     } else if (n_tiles <= 256 && EPI != EPI_LOGITS && EPI != EPI_SWIGLU) {
-      hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, 4, 2>), dim3((n_tiles + 1) / 2, (a.M + 31) / 32), block, 0, s, a);
+      go<T, EPI, 2, 4, 2>(a, g, dim3((n_tiles + 1) / 2, (M + 31) / 32), s);
     } else {
-      const unsigned mb = (unsigned)((a.M + 63) / 64);
+      const unsigned mb = (unsigned)((M + 63) / 64);
       if constexpr (EPI == EPI_LOGITS)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 2, 4>), dim3((n_tiles + 3) / 4, mb), block, 0, s, a);
+        go<T, EPI, 4, 2, 4>(a, g, dim3((n_tiles + 3) / 4, mb), s);
       else if constexpr (EPI == EPI_SWIGLU)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 2, 2>), dim3((n_tiles + 1) / 2, mb), block, 0, s, a);
+        go<T, EPI, 4, 2, 2>(a, g, dim3((n_tiles + 1) / 2, mb), s);
       else
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, 4, 4, 1>), dim3(n_tiles, mb), block, 0, s, a);
+        go<T, EPI, 4, 4, 1>(a, g, dim3(n_tiles, mb), s);
     }
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipStream_t s) {
+  if (m_blocks <= 0) return hipErrorInvalidValue;
   if (dtype == 1) {
     switch (epi) {
-      case EPI_PLAIN: return launch_t<bf16, EPI_PLAIN>(a, m_blocks, s);
-      case EPI_QKV: return launch_t<bf16, EPI_QKV>(a, m_blocks, s);
-      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, m_blocks, s);
-      case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, m_blocks, s);
-      case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, m_blocks, s);
-      case EPI_BIAS_SILU: return launch_t<bf16, EPI_BIAS_SILU>(a, m_blocks, s);
+      case EPI_PLAIN: return launch_t<bf16, EPI_PLAIN>(a, nullptr, a.M, s);
+      case EPI_QKV: return launch_t<bf16, EPI_QKV>(a, nullptr, a.M, s);
+      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, nullptr, a.M, s);
+      case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, nullptr, a.M, s);
+      case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, nullptr, a.M, s);
+      case EPI_BIAS_SILU: return launch_t<bf16, EPI_BIAS_SILU>(a, nullptr, a.M, s);
     }
   } else {
     switch (epi) {
-      case EPI_PLAIN: return launch_t<float, EPI_PLAIN>(a, m_blocks, s);
-      case EPI_QKV: return launch_t<float, EPI_QKV>(a, m_blocks, s);
-      case EPI_RESID: return launch_t<float, EPI_RESID>(a, m_blocks, s);
-      case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, m_blocks, s);
-      case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, m_blocks, s);
-      case EPI_BIAS_SILU: return launch_t<float, EPI_BIAS_SILU>(a, m_blocks, s);
+      case EPI_PLAIN: return launch_t<float, EPI_PLAIN>(a, nullptr, a.M, s);
+      case EPI_QKV: return launch_t<float, EPI_QKV>(a, nullptr, a.M, s);
+      case EPI_RESID: return launch_t<float, EPI_RESID>(a, nullptr, a.M, s);
+      case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, nullptr, a.M, s);
+      case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, nullptr, a.M, s);
+      case EPI_BIAS_SILU: return launch_t<float, EPI_BIAS_SILU>(a, nullptr, a.M, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+// Up to MAX_SEGS segments per launch; a lone segment as a plain launch.
+template <typename T, int EPI>
+static hipError_t launch_seg_t(const GemmArgs &a, const GemmSeg *segs, int n, hipStream_t s) {
+  for (int i0 = 0; i0 < n; i0 += MAX_SEGS) {
+    const int c = n - i0 < MAX_SEGS ? n - i0 : MAX_SEGS;
+    hipError_t e;
+    if (c == 1) {
+      GemmArgs b = a;
+      gemm_seg_view<T, EPI>(b, segs[i0]);
+      e = launch_t<T, EPI>(b, nullptr, b.M, s);
+    } else {
+      GemmSegs g{};
+      g.n = c;
+      int M = 0;
+      for (int i = 0; i < c; ++i) {
+        g.s[i] = segs[i0 + i];
+        M = g.s[i].M > M ? g.s[i].M : M;
+      }
+      e = launch_t<T, EPI>(a, &g, M, s);
+    }
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_gemm_seg(int dtype, int epi, const GemmArgs &a, const GemmSeg *segs, int n, hipStream_t s) {
+  if (n < 1 || segs == nullptr) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (segs[i].M < 1 || segs[i].r0 < 0) return hipErrorInvalidValue;
+  if (dtype == 1) {
+    switch (epi) {
+      case EPI_QKV: return launch_seg_t<bf16, EPI_QKV>(a, segs, n, s);
+      case EPI_RESID: return launch_seg_t<bf16, EPI_RESID>(a, segs, n, s);
+      case EPI_SWIGLU: return launch_seg_t<bf16, EPI_SWIGLU>(a, segs, n, s);
+    }
+  } else {
+    switch (epi) {
+      case EPI_QKV: return launch_seg_t<float, EPI_QKV>(a, segs, n, s);
+      case EPI_RESID: return launch_seg_t<float, EPI_RESID>(a, segs, n, s);
+      case EPI_SWIGLU: return launch_seg_t<float, EPI_SWIGLU>(a, segs, n, s);
     }
   }
   return hipErrorInvalidValue;

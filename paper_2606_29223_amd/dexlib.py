@@ -50,7 +50,7 @@ class DexConfig(ctypes.Structure):
         ("max_context", ctypes.c_int32), ("hip_stream", ctypes.c_void_p),
         ("stage_streams", ctypes.c_int32), ("temperature", ctypes.c_float),
         ("sample_seed", ctypes.c_uint64), ("adapter_dim", ctypes.c_int32),
-        ("adapters", ctypes.POINTER(ctypes.c_void_p)),
+        ("adapters", ctypes.POINTER(ctypes.c_void_p)), ("stage_grouping", ctypes.c_int32),
     ]
 
 
@@ -200,7 +200,7 @@ class Decoder:
 
     def __init__(self, cfg: dict, dev_weights: dict, explored=None, width_cap=None, decs=None,
                  batch=None, max_context=None, stream=None, stage_streams=0, temperature=0.0, seed=0,
-                 adapters=None):
+                 adapters=None, stage_grouping=0):
         import torch
         self.lib = load()
         self.cfg = cfg
@@ -234,6 +234,7 @@ class Decoder:
         self.stream = stream if stream is not None else torch.cuda.Stream()
         c.hip_stream = self.stream.cuda_stream
         c.stage_streams = int(stage_streams)
+        c.stage_grouping = int(stage_grouping)
         c.temperature = float(temperature)
         c.sample_seed = int(seed) & ((1 << 64) - 1)
         # inducing adapters: device tensors "adapters.{k}.{part}" for the

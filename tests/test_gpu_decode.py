@@ -450,29 +450,36 @@ def test_gqa128_prefill_ragged_prompts(P, G):
         assert seen == T - 1
 
 
-def test_stage_streams_do_not_change_results():
-    """Spreading a round's stages over several streams changes only the
-    schedule: tokens, lattice traces and every row's exit logits are the same
-    bits as with all stages on one stream (batch 3, width 4, 12 layers)."""
+@pytest.mark.parametrize("name", [SMALL, TINY])
+def test_stage_schedules_do_not_change_results(name):
+    """Grouped launches (a lane's stages in step, each kernel launched once
+    per layer step for all of them) on one lane and on three, and per-stage
+    launches on one stream and spread over four, change only the schedule:
+    tokens, lattice traces and every row's exit logits are the same bits
+    (batch 3; the bf16 model takes the grouped matrix-core attention, the
+    fp32 model one attention launch per stage inside the grouped sweep)."""
     torch = torch_cuda()
     from paper_2606_29223_amd import dexlib
-    cfg = configs.get(SMALL, batch=3, prompt_seeds=[8101, 8102, 8103])
+    cfg = configs.get(name, batch=3, prompt_seeds=[8101, 8102, 8103])
     prompt = gen.prompts(cfg)
     T = 24
+    W = cfg["width_cap"] or 2 ** (len(cfg["explored"]) - 1)
     out = []
-    for lanes in (1, 4):
-        dec = dexlib.Decoder(cfg, device_weights(SMALL), max_context=cfg["prompt_len"] + T, stage_streams=lanes)
-        tap = torch.empty((dec.batch * cfg["width_cap"], cfg["vocab"]), dtype=torch.float32, device="cuda")
+    for grouping, lanes in ((0, 1), (0, 3), (-1, 1), (-1, 4)):
+        dec = dexlib.Decoder(cfg, device_weights(name), max_context=cfg["prompt_len"] + T, stage_streams=lanes,
+                             stage_grouping=grouping)
+        tap = torch.empty((dec.batch * W, cfg["vocab"]), dtype=torch.float32, device="cuda")
         dec.set_logits_tap(tap)
         out.append(_run(dec, prompt, T, tap=tap))
         dec.close()
-    (t1, r1), (t4, r4) = out
-    assert np.array_equal(t1, t4)
-    assert len(r1) == len(r4)
-    for a, b in zip(r1, r4):
-        assert a["rows"] == b["rows"] and a["kstar"] == b["kstar"] and a["collapse"] == b["collapse"]
-        assert all(np.array_equal(x, y) for x, y in zip(a["lattice"], b["lattice"]))
-        assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+    t0, r0 = out[0]
+    for t1, r1 in out[1:]:
+        assert np.array_equal(t0, t1)
+        assert len(r0) == len(r1)
+        for a, b in zip(r0, r1):
+            assert a["rows"] == b["rows"] and a["kstar"] == b["kstar"] and a["collapse"] == b["collapse"]
+            assert all(np.array_equal(x, y) for x, y in zip(a["lattice"], b["lattice"]))
+            assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
 
 
 def test_small_bf16_long_context_merged_blocks():
