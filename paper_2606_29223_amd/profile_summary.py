@@ -38,6 +38,12 @@ SHORT = {
     "gemm_kernel<unsigned short, 3, 1,": "gate/up (bf16, M<=16)",
     "gemm_kernel<unsigned short, 4, 1,": "lm-head (bf16, M<=16)",
 }
+# grouped launches (one segment per stage on grid z): listed per segment
+SHORT_SEG = {
+    "gemm_seg_kernel<unsigned short, 1, 1,": "qkv grouped, per segment",
+    "gemm_seg_kernel<unsigned short, 2, 1,": "o-proj / down grouped, per segment",
+    "gemm_seg_kernel<unsigned short, 3, 1,": "gate/up grouped, per segment",
+}
 
 
 def code_text(src: str) -> str:
@@ -100,7 +106,8 @@ def stats(args):
         lines.append(f"{_short(r['Name'])[:58]:58s} {r['Calls']:>7s} {float(r['AverageNs']) / 1e3:9.2f} "
                      f"{float(r['TotalDurationNs']) / 1e6:9.2f} {float(r['Percentage']):6.1f}")
     if trace:
-        lines += ["", "decode launches (median duration; decode = M <= 16 GEMMs and the decode attention kernels)"]
+        lines += ["", "decode launches (median duration; decode = M <= 16 GEMMs and the decode attention kernels;",
+                  "a grouped GEMM launch counts once per segment, at its duration / segments)"]
         groups = {}
         for t in trace:
             n = _short(t["Kernel_Name"])
@@ -109,8 +116,16 @@ def stats(args):
             for k, v in SHORT.items():
                 if n.startswith(k):
                     key = v
+            for k, v in SHORT_SEG.items():
+                if n.startswith(k):
+                    key = v
+                    segs = max(int(t.get("Grid_Size_Z") or 1), 1)
+                    groups.setdefault(key, []).extend([dur / segs] * segs)
+                    key = None
             if n.startswith("attn_mfma_kernel") or (n.startswith("attn_kernel") and int(t["Grid_Size_X"]) <= 256 * 64):
                 key = "attention (decode)"
+            if n.startswith("attn_mfma_seg_kernel"):
+                key = "attention grouped, per launch"
             if n.startswith("combine_kernel") and int(t["Grid_Size_X"]) <= 256 * 64:
                 key = "attention combine (decode)"
             if key:
