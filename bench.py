@@ -299,6 +299,12 @@ def main():
             if ent and ks.get("source") == csrc_source_hash() and ks.get("config") == cfg["name"]:
                 roofline["rocprof"] = {"avg_launch_us": round(ent["avg_us"], 2), "launches": ent["launches"],
                                        "frac": round(bytes_per / (ent["avg_us"] * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                                       "median_launch_us": round(ent["median_us"], 2),
+                                       "median_frac": round(bytes_per / (ent["median_us"] * 1e-6) / 1e9
+                                                            / PEAK_HBM_GBS, 4),
+                                       "note": "single-layer launches of the class in the traced run; launches "
+                                               "of concurrent stage lanes overlap and share HBM, which lengthens "
+                                               "some (the mean) but not the typical one (the median)",
                                        "profile": os.path.relpath(args.kernel_stats_json, ROOT)}
         except (OSError, ValueError, KeyError):
             pass
