@@ -611,6 +611,7 @@ static __host__ __device__ inline void attn_seg_view(AttnArgs &a, const AttnSeg 
   a.grp_row0 += sg.g0;
   a.grp_nrows += sg.g0;
   a.grp_seq += sg.g0;
+  if (a.grp_nc != nullptr) a.grp_nc += sg.g0;
   a.n_rows = sg.M;
   a.n_splits = sg.n_splits;
   a.part = (T *)a.part + r0 * a.n_heads * a.jmax * a.head_dim;

@@ -78,7 +78,12 @@ __device__ __forceinline__ void wave_lds_sync() {
 //                positions, so two splits.  Dispatched first.
 //   group items  (row group, split): every row of the group that reaches
 //                the split and has no chain positions in it, committed
-//                keys only.
+//                keys only.  A split below the group's committed length
+//                (every split but the last at long context) takes all of
+//                the group's rows and needs none of their positions, so
+//                its keys are requested right after the group's table
+//                entries instead of after a further round trip for the
+//                rows' positions.
 // An MFMA 16x16x32 bf16 operand fragment from a key-major LDS tile with two
 // transpose reads (ds_read_b64_tr_b16).  Within each quarter-wave, lane j
 // receives element i from the address of lane 4 i + j / 4 at offset j % 4;
@@ -130,34 +135,44 @@ __device__ void attn_mfma_item(const AttnArgs &a, int item, int kvh, uint16_t (*
     seq = a.grp_seq[gi];
     const int nr = a.grp_nrows[gi];
     const int s0 = split * ATT_SPLIT, s1 = s0 + ATT_SPLIT - 1;
-    // lane rr holds row rr of the group (at most 64 rows)
-    const bool lr = lane < nr;
-    const int mypos = lr ? a.row_pos[r0 + lane] : -1;
-    const int mync = lr ? a.row_nc[r0 + lane] : 0;
-    int maxpos = mypos, ncmax = mync;
+    if (a.grp_nc != nullptr && s1 < a.grp_nc[gi]) {
+      // a split wholly inside the group's committed prefix: every row of the
+      // group reaches past it and has no chain position in it, so all of
+      // them take every key -- the decisions below, read off the group alone
+      n_pass = nr;
+      if (lane < nr) { prow[lane] = lane; ppos[lane] = INT_MAX; }
+      tn = ATT_SPLIT;
+      full = true;
+    } else {
+      // lane rr holds row rr of the group (at most 64 rows)
+      const bool lr = lane < nr;
+      const int mypos = lr ? a.row_pos[r0 + lane] : -1;
+      const int mync = lr ? a.row_nc[r0 + lane] : 0;
+      int maxpos = mypos, ncmax = mync;
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      maxpos = max(maxpos, __shfl_xor(maxpos, o, 64));
-      ncmax = max(ncmax, __shfl_xor(ncmax, o, 64));
-    }
-    if (s0 > maxpos) return;
-    // a row whose chain positions fall in this split gets it from its chain
-    // item; the pass takes the group's other rows that reach the split
-    const bool chain_here = lr && max(mync, s0) <= min(mypos, s1);
-    const bool in_pass = mypos >= s0 && !chain_here;
-    const unsigned long long reach = __ballot(in_pass);
-    if (reach == 0ull) return;
-    n_pass = __popcll(reach);
-    if (in_pass) {
-      const int k = __popcll(reach & ((1ull << lane) - 1ull));
-      prow[k] = lane;
-      ppos[k] = mypos;
-    }
-    tn = max(0, min(ATT_SPLIT, ncmax - s0));
-    int minpos = in_pass ? mypos : INT_MAX;
+      for (int o = 32; o >= 1; o >>= 1) {
+        maxpos = max(maxpos, __shfl_xor(maxpos, o, 64));
+        ncmax = max(ncmax, __shfl_xor(ncmax, o, 64));
+      }
+      if (s0 > maxpos) return;
+      // a row whose chain positions fall in this split gets it from its chain
+      // item; the pass takes the group's other rows that reach the split
+      const bool chain_here = lr && max(mync, s0) <= min(mypos, s1);
+      const bool in_pass = mypos >= s0 && !chain_here;
+      const unsigned long long reach = __ballot(in_pass);
+      if (reach == 0ull) return;
+      n_pass = __popcll(reach);
+      if (in_pass) {
+        const int k = __popcll(reach & ((1ull << lane) - 1ull));
+        prow[k] = lane;
+        ppos[k] = mypos;
+      }
+      tn = max(0, min(ATT_SPLIT, ncmax - s0));
+      int minpos = in_pass ? mypos : INT_MAX;
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) minpos = min(minpos, __shfl_xor(minpos, o, 64));
-    full = tn == ATT_SPLIT && s1 <= minpos;
+      for (int o = 32; o >= 1; o >>= 1) minpos = min(minpos, __shfl_xor(minpos, o, 64));
+      full = tn == ATT_SPLIT && s1 <= minpos;
+    }
   }
   wave_lds_sync();
   const int s0 = split * ATT_SPLIT;

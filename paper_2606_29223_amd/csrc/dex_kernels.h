@@ -132,8 +132,9 @@ struct AttnArgs {
   int ldq;
   const void *kc, *vc;        // this layer's cache base
   int kv_entries, n_kv_heads, n_heads, head_dim, batch;
-  // row groups: consecutive rows of one sequence
-  const int *grp_row0, *grp_nrows, *grp_seq;
+  // row groups: consecutive rows of one sequence that share their committed
+  // prefix; grp_nc (nullable) is that prefix's length
+  const int *grp_row0, *grp_nrows, *grp_seq, *grp_nc;
   const int *row_pos, *row_nc, *row_chain_off, *chain;
   const int *row_seq;         // sequence of each row (matrix-core kernel)
   int n_rows;                 // rows of the launch (matrix-core kernel)

@@ -366,7 +366,7 @@ inline int slot_global(const dex_ctx *ctx, int seq, const Seq &s, int slot) {
 // ------------------------------------------------------- kernel drivers
 struct StageTables {
   const int *seq, *pos, *entry, *bnd, *tok, *nc, *chain_off, *chain, *mask_n, *mask_tok, *cand_idx;
-  const int *g_row0, *g_nrows, *g_seq;
+  const int *g_row0, *g_nrows, *g_seq, *g_nc;
   int n_groups;
   int n_splits;         // 64-key splits up to the stage's deepest row
   double attn_bytes;    // keys/values a layer's attention reads (algorithmic)
@@ -401,7 +401,7 @@ dex_status run_layers(dex_ctx *ctx, hipStream_t st, int first_layer, int last_la
       a.q = q; a.ldq = H * hd;
       a.kc = (char *)ctx->kc + l * layer_kv; a.vc = (char *)ctx->vc + l * layer_kv;
       a.kv_entries = ctx->E; a.n_kv_heads = Hkv; a.n_heads = H; a.head_dim = hd; a.batch = ctx->B;
-      a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq;
+      a.grp_row0 = t.g_row0; a.grp_nrows = t.g_nrows; a.grp_seq = t.g_seq; a.grp_nc = t.g_nc;
       a.row_pos = t.pos; a.row_nc = t.nc; a.row_chain_off = t.chain_off; a.chain = t.chain;
       a.row_seq = t.seq; a.n_rows = M;
       a.part = apart; a.stat = split_stats(apart, M, H, jmax, hd);
@@ -577,12 +577,12 @@ struct AttnCall {
 // Offsets (in ints) of the device row tables, the row-group count, the split
 // count and the split partials' size of one call.
 struct AttnTab {
-  size_t o_pos, o_nc, o_seq, o_coff, o_g0, o_gn, o_gs, o_chain, n_ints;
+  size_t o_pos, o_nc, o_seq, o_coff, o_g0, o_gn, o_gs, o_gc, o_chain, n_ints;
   int ng, n_splits;
   size_t part_bytes;
 };
 
-size_t attention_table_ints(int n_rows, int chain_len) { return 7 * (size_t)n_rows + (size_t)chain_len + 1; }
+size_t attention_table_ints(int n_rows, int chain_len) { return 8 * (size_t)n_rows + (size_t)chain_len + 1; }
 
 // Validates a call on the host (nothing is launched for a bad one) and
 // writes its row tables to tab (cap ints, at least attention_table_ints):
@@ -626,11 +626,12 @@ dex_status attention_tables(const AttnCall &c, int *tab, size_t cap, AttnTab *t)
     r = e;
   }
   t->ng = ng;
-  t->o_gn = t->o_g0 + ng; t->o_gs = t->o_gn + ng; t->o_chain = t->o_gs + ng;
+  t->o_gn = t->o_g0 + ng; t->o_gs = t->o_gn + ng; t->o_gc = t->o_gs + ng; t->o_chain = t->o_gc + ng;
   for (int g = 0; g < ng; ++g) {
     const int e = g + 1 < ng ? g0[g + 1] : R;
     tab[t->o_gn + g] = e - g0[g];
     tab[t->o_gs + g] = c.row_seq[g0[g]];
+    tab[t->o_gc + g] = c.row_nc[g0[g]];
   }
   if (c.chain_len > 0) std::copy(c.chain, c.chain + c.chain_len, tab + t->o_chain);
   else tab[t->o_chain] = 0;
@@ -646,7 +647,7 @@ hipError_t launch_attention_call(const AttnCall &c, const AttnTab &t, const int 
   AttnArgs a{};
   a.q = c.q; a.ldq = c.n_heads * c.head_dim; a.kc = c.k_cache; a.vc = c.v_cache; a.kv_entries = c.kv_entries;
   a.n_kv_heads = c.n_kv_heads; a.n_heads = c.n_heads; a.head_dim = c.head_dim; a.batch = c.batch;
-  a.grp_row0 = dtab + t.o_g0; a.grp_nrows = dtab + t.o_gn; a.grp_seq = dtab + t.o_gs;
+  a.grp_row0 = dtab + t.o_g0; a.grp_nrows = dtab + t.o_gn; a.grp_seq = dtab + t.o_gs; a.grp_nc = dtab + t.o_gc;
   a.row_pos = dtab + t.o_pos; a.row_nc = dtab + t.o_nc; a.row_chain_off = dtab + t.o_coff;
   a.chain = dtab + t.o_chain; a.row_seq = dtab + t.o_seq; a.n_rows = c.n_rows; a.part = part;
   a.stat = split_stats(part, c.n_rows, c.n_heads, t.n_splits, c.head_dim);
@@ -668,7 +669,7 @@ hipError_t launch_attention_call(const AttnCall &c, const AttnTab &t, const int 
 constexpr size_t kScratchBytes = 64ull << 20;
 constexpr size_t kScratchTableBytes = 256ull << 10;
 constexpr int kNoallocMaxChain = 16384;
-constexpr size_t kNoallocTableInts = 7 * DEX_MAX_ROWS + kNoallocMaxChain + 1;
+constexpr size_t kNoallocTableInts = 8 * DEX_MAX_ROWS + kNoallocMaxChain + 1;
 static_assert(kNoallocTableInts * 4 <= kScratchTableBytes, "row tables fit their scratch region");
 
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
@@ -1254,7 +1255,8 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   int *t_chain = t_mask + R * N;           // [R * CH_MAX]
   int *t_g0 = t_chain + R * ctx->CH_MAX;   // groups (stage-local row0), up to R
   int *t_gn = t_g0 + R, *t_gs = t_gn + R;
-  int *t_rcommit = t_gs + R;               // [R] commit slot of a row completing its anchor, else -1
+  int *t_gnc = t_gs + R;                   // committed prefix length of each group's rows
+  int *t_rcommit = t_gnc + R;              // [R] commit slot of a row completing its anchor, else -1
   std::vector<int> stage_r0(N + 1, 0), stage_g0(N + 1, 0);
   int chain_used = 0, ngroups = 0;
   const int G = ctx->H / ctx->Hkv;
@@ -1295,6 +1297,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
       t_g0[ngroups] = r - stage_r0[k];
       t_gn[ngroups] = e - r;
       t_gs[ngroups] = rows[r].seq;
+      t_gnc[ngroups] = t_nc[r];
       ++ngroups;
       r = e;
     }
@@ -1368,6 +1371,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     t.seq = dptr(t_seq) + r0; t.pos = dptr(t_pos) + r0; t.entry = dptr(t_entry) + r0; t.bnd = dptr(t_bnd) + r0;
     t.tok = dptr(t_tok) + r0; t.nc = dptr(t_nc) + r0; t.chain_off = dptr(t_coff) + r0; t.chain = dptr(t_chain);
     t.g_row0 = dptr(t_g0) + stage_g0[k]; t.g_nrows = dptr(t_gn) + stage_g0[k]; t.g_seq = dptr(t_gs) + stage_g0[k];
+    t.g_nc = dptr(t_gnc) + stage_g0[k];
     t.n_groups = stage_g0[k + 1] - stage_g0[k];
     t.attn_bytes = 0.0;
     int stage_maxpos = 0;
@@ -1473,7 +1477,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
         AttnArgs a{};
         a.q = ctx->q_w; a.ldq = H * hd;
         a.kv_entries = ctx->E; a.n_kv_heads = Hkv; a.n_heads = H; a.head_dim = hd; a.batch = B;
-        a.grp_row0 = dptr(t_g0); a.grp_nrows = dptr(t_gn); a.grp_seq = dptr(t_gs);
+        a.grp_row0 = dptr(t_g0); a.grp_nrows = dptr(t_gn); a.grp_seq = dptr(t_gs); a.grp_nc = dptr(t_gnc);
         a.row_pos = dptr(t_pos); a.row_nc = dptr(t_nc); a.row_chain_off = dptr(t_coff); a.chain = dptr(t_chain);
         a.row_seq = dptr(t_seq);
         a.part = ctx->attn_part; a.stat = stat_all;
