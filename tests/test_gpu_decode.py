@@ -482,6 +482,40 @@ def test_stage_schedules_do_not_change_results(name):
             assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
 
 
+def test_grouped_lane_longer_than_one_launch():
+    """Every layer of the 12-layer model explored (12 stages, width 16,
+    batch 2) on one grouped lane: a layer step's segment list outgrows what
+    one launch takes and goes out as several launches.  Tokens, lattice
+    traces and every exit logit equal per-stage launches bit for bit, and
+    the committed tokens equal plain AR's."""
+    torch = torch_cuda()
+    from paper_2606_29223_amd import dexlib
+    cfg = configs.get(SMALL, batch=2, explored=list(range(1, 13)), width_cap=16, prompt_seeds=[8201, 8202])
+    prompt = gen.prompts(cfg)
+    T = 20
+    out, most = [], 0
+    for grouping in (0, -1):
+        dec = dexlib.Decoder(cfg, device_weights(SMALL), max_context=cfg["prompt_len"] + T, stage_streams=1,
+                             stage_grouping=grouping)
+        tap = torch.empty((dec.batch * 16, cfg["vocab"]), dtype=torch.float32, device="cuda")
+        dec.set_logits_tap(tap)
+        toks, rounds = _run(dec, prompt, T, tap=tap)
+        dec.close()
+        out.append((toks, rounds))
+        most = max(most, max(len({r[2] for r in rd["rows"]}) for rd in rounds))
+    assert most > 8                     # some round ran more stages than one launch takes
+    (t0, r0), (t1, r1) = out
+    assert np.array_equal(t0, t1) and len(r0) == len(r1)
+    for a, b in zip(r0, r1):
+        assert a["rows"] == b["rows"] and a["kstar"] == b["kstar"]
+        assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+    ar = dexlib.Decoder(cfg, device_weights(SMALL), explored=[cfg["n_layers"]], width_cap=1,
+                        max_context=cfg["prompt_len"] + T)
+    ar_toks, _ = _run(ar, prompt, T, collapse=False)
+    ar.close()
+    assert np.array_equal(t0, ar_toks)
+
+
 def test_small_bf16_long_context_merged_blocks():
     """A 2600-token prompt (41 key splits, several beyond one wave's reach of
     64 rows' groups): DEX still equals plain AR bit for bit, and the tokens
