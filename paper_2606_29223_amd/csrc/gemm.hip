@@ -323,10 +323,47 @@ static void go(const GemmArgs &a, const GemmSegs *g, dim3 grid, hipStream_t s) {
   hipLaunchKernelGGL((gemm_kernel<T, EPI, MB, U, NTW>), grid, dim3(GEMM_THREADS), 0, s, a);
 }
 
-// The configuration for M rows (a grouped launch: its largest segment's).
+// Weight tiles per workgroup of a projection with 256 (O, down) or 384 (QKV)
+// tiles at up to 32 rows over nseg segments: every activation load feeds
+// NTW tiles, which pays from 5 rows on once the grid still fills the chip;
+// at 1-4 rows a grouped launch keeps one tile with a shallower prefetch
+// (measured per class, row count and segment count on the 32-layer d4096
+// model, lone QKV launches at 1-4 rows inside the decode step; 0: the
+// general table).
+static int proj_tiles_per_wg(int n_tiles, int M, int nseg) {
+  if (M > 32 || n_tiles < 256 || n_tiles > 384) return 0;
+  const bool qkv = n_tiles > 256;
+  if (nseg == 1) return qkv && M > 4 ? 2 : 0;
+  if (M <= 4) return 1;
+  if (nseg == 2) return qkv ? 4 : 2;
+  if (nseg <= 4) return qkv ? 2 : (nseg == 4 && M <= 8 ? 2 : 4);
+  return 4;
+}
+
+// The configuration for M rows (a grouped launch of nseg segments: its
+// largest segment's).
 template <typename T, int EPI>
-static hipError_t launch_t(const GemmArgs &a, const GemmSegs *g, int M, hipStream_t s) {
+static hipError_t launch_t(const GemmArgs &a, const GemmSegs *g, int M, int nseg, hipStream_t s) {
   const int n_tiles = (a.N + 15) / 16;
+  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
+    const int ntw = proj_tiles_per_wg(n_tiles, M, nseg);
+    if (ntw == 1) {
+      go<T, EPI, 1, 2, 1>(a, g, dim3(n_tiles, 1), s);
+      return hipGetLastError();
+    }
+    if (ntw > 0 && M <= 16) {
+      if (ntw == 4) go<T, EPI, 1, 2, 4>(a, g, dim3((n_tiles + 3) / 4, 1), s);
+      else if (nseg == 1) go<T, EPI, 1, 8, 2>(a, g, dim3((n_tiles + 1) / 2, 1), s);
+      else go<T, EPI, 1, 4, 2>(a, g, dim3((n_tiles + 1) / 2, 1), s);
+      return hipGetLastError();
+    }
+    if (ntw > 0) {
+      if (ntw == 4) go<T, EPI, 2, 2, 4>(a, g, dim3((n_tiles + 3) / 4, 1), s);
+      else if (EPI == EPI_QKV && nseg > 1) go<T, EPI, 2, 2, 2>(a, g, dim3((n_tiles + 1) / 2, 1), s);
+      else go<T, EPI, 2, 4, 2>(a, g, dim3((n_tiles + 1) / 2, 1), s);
+      return hipGetLastError();
+    }
+  }
   if (M <= 16) {
     // deeper prefetch when a workgroup per CU streams a long tile, shallower
     // when many workgroups share each CU (measured on the 4096-wide layers);
@@ -374,21 +411,21 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs &a, int m_blocks, hipS
   if (m_blocks <= 0) return hipErrorInvalidValue;
   if (dtype == 1) {
     switch (epi) {
-      case EPI_PLAIN: return launch_t<bf16, EPI_PLAIN>(a, nullptr, a.M, s);
-      case EPI_QKV: return launch_t<bf16, EPI_QKV>(a, nullptr, a.M, s);
-      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, nullptr, a.M, s);
-      case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, nullptr, a.M, s);
-      case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, nullptr, a.M, s);
-      case EPI_BIAS_SILU: return launch_t<bf16, EPI_BIAS_SILU>(a, nullptr, a.M, s);
+      case EPI_PLAIN: return launch_t<bf16, EPI_PLAIN>(a, nullptr, a.M, 1, s);
+      case EPI_QKV: return launch_t<bf16, EPI_QKV>(a, nullptr, a.M, 1, s);
+      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, nullptr, a.M, 1, s);
+      case EPI_SWIGLU: return launch_t<bf16, EPI_SWIGLU>(a, nullptr, a.M, 1, s);
+      case EPI_LOGITS: return launch_t<bf16, EPI_LOGITS>(a, nullptr, a.M, 1, s);
+      case EPI_BIAS_SILU: return launch_t<bf16, EPI_BIAS_SILU>(a, nullptr, a.M, 1, s);
     }
   } else {
     switch (epi) {
-      case EPI_PLAIN: return launch_t<float, EPI_PLAIN>(a, nullptr, a.M, s);
-      case EPI_QKV: return launch_t<float, EPI_QKV>(a, nullptr, a.M, s);
-      case EPI_RESID: return launch_t<float, EPI_RESID>(a, nullptr, a.M, s);
-      case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, nullptr, a.M, s);
-      case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, nullptr, a.M, s);
-      case EPI_BIAS_SILU: return launch_t<float, EPI_BIAS_SILU>(a, nullptr, a.M, s);
+      case EPI_PLAIN: return launch_t<float, EPI_PLAIN>(a, nullptr, a.M, 1, s);
+      case EPI_QKV: return launch_t<float, EPI_QKV>(a, nullptr, a.M, 1, s);
+      case EPI_RESID: return launch_t<float, EPI_RESID>(a, nullptr, a.M, 1, s);
+      case EPI_SWIGLU: return launch_t<float, EPI_SWIGLU>(a, nullptr, a.M, 1, s);
+      case EPI_LOGITS: return launch_t<float, EPI_LOGITS>(a, nullptr, a.M, 1, s);
+      case EPI_BIAS_SILU: return launch_t<float, EPI_BIAS_SILU>(a, nullptr, a.M, 1, s);
     }
   }
   return hipErrorInvalidValue;
@@ -403,7 +440,7 @@ static hipError_t launch_seg_t(const GemmArgs &a, const GemmSeg *segs, int n, hi
     if (c == 1) {
       GemmArgs b = a;
       gemm_seg_view<T, EPI>(b, segs[i0]);
-      e = launch_t<T, EPI>(b, nullptr, b.M, s);
+      e = launch_t<T, EPI>(b, nullptr, b.M, 1, s);
     } else {
       GemmSegs g{};
       g.n = c;
@@ -412,7 +449,7 @@ static hipError_t launch_seg_t(const GemmArgs &a, const GemmSeg *segs, int n, hi
         g.s[i] = segs[i0 + i];
         M = g.s[i].M > M ? g.s[i].M : M;
       }
-      e = launch_t<T, EPI>(a, &g, M, s);
+      e = launch_t<T, EPI>(a, &g, M, c, s);
     }
     if (e != hipSuccess) return e;
   }
