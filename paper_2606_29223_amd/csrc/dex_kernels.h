@@ -271,12 +271,17 @@ hipError_t launch_attention_seg(int dtype, const AttnArgs &a, const AttnSeg *seg
 
 struct PrepArgs {
   int M, d, n_part;
-  int from_embed;             // 1: h = E[token]; 0: h = boundary[src]
+  int embed_rows;             // rows [0, embed_rows): h = E[token]; the others h = boundary[src]
   const int *row_tok;         // embed token per row
   const int *row_src;         // boundary index per row
   const void *embed;
   const float *bnd_h, *bnd_part;
   const float *g;             // gain of the first RMSNorm the rows meet
+  // n_seg > 0: segments of consecutive rows (one per stage of a grouped
+  // lane), rows [seg_end[k-1], seg_end[k]) meeting gain seg_g[k] instead of g
+  int n_seg;
+  int seg_end[MAX_SEGS];
+  const float *seg_g[MAX_SEGS];
   float *h, *part;            // [M][d], [M][n_part]
   void *xb;                   // [M][d] (T)
   const int *row_out;         // nullable: write h/part to row_out[m] instead of m

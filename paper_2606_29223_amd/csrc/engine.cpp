@@ -465,7 +465,7 @@ dex_status exit_prep(dex_ctx *ctx, int r0, int M, const int *row_src, const floa
                      const float *g) {
   if (M <= 0) return DEX_OK;
   PrepArgs p{};
-  p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = 0;
+  p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.embed_rows = 0;
   p.row_src = row_src + r0; p.bnd_h = src_h; p.bnd_part = src_part; p.g = g;
   p.h = ctx->ex_h + (size_t)r0 * ctx->d; p.part = ctx->ex_part + (size_t)r0 * ctx->n_part;
   p.xb = (char *)ctx->ex_xb + (size_t)r0 * ctx->d * ctx->es;
@@ -1091,7 +1091,7 @@ dex_status dex_prefill(dex_ctx *ctx, const int32_t *prompts, int32_t P, int32_t 
 
   {
     PrepArgs p{};
-    p.M = (int)M; p.d = d; p.n_part = ctx->n_part; p.from_embed = 1; p.row_tok = d_tok; p.embed = ctx->embed;
+    p.M = (int)M; p.d = d; p.n_part = ctx->n_part; p.embed_rows = (int)M; p.row_tok = d_tok; p.embed = ctx->embed;
     p.g = (const float *)LW(ctx, 0, DEX_P_ATTN_NORM); p.h = h; p.part = part; p.xb = xb;
     HIPCHK(launch_prep(ctx->dtype, p, ctx->stream));
   }
@@ -1361,7 +1361,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
   // a stage's tables, its share of the round's sums, and the launch that
   // gives its rows their first RMSNorm input (from the embedding or the
   // boundary state their slot reached)
-  auto stage_prologue = [&](int k, StageTables &t, hipStream_t lst) -> dex_status {
+  auto stage_prologue = [&](int k, StageTables &t, hipStream_t lst, bool prep) -> dex_status {
     const int r0 = stage_r0[k], M = stage_r0[k + 1] - r0;
     LaneSum &acc = lane_sum[stage_lane[k]];
     const std::vector<int> &ls = ctx->stage_layers[k];
@@ -1384,9 +1384,9 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     t.n_splits = std::min(ctx->jmax, stage_maxpos / ATT_SPLIT + 1);
     t.attn_bytes += (double)M * ctx->H * ctx->hd * (4.0 + ctx->es);
     acc.attn_bytes += t.attn_bytes * (double)ls.size();
-    {
+    if (prep) {
       PrepArgs p{};
-      p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.from_embed = (k == 0);
+      p.M = M; p.d = ctx->d; p.n_part = ctx->n_part; p.embed_rows = (k == 0) ? M : 0;
       p.row_tok = t.tok; p.row_src = t.bnd; p.embed = ctx->embed; p.bnd_h = ctx->bnd_h; p.bnd_part = ctx->bnd_part;
       p.g = (const float *)LW(ctx, ls.front(), DEX_P_ATTN_NORM);
       p.h = ctx->h_w + (size_t)r0 * ctx->d; p.part = ctx->part_w + (size_t)r0 * ctx->n_part;
@@ -1401,7 +1401,7 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     const hipStream_t lst = multi ? ctx->lane_st[stage_lane[k]] : ctx->stream;
     const std::vector<int> &ls = ctx->stage_layers[k];
     StageTables t{};
-    const dex_status ps = stage_prologue(k, t, lst);
+    const dex_status ps = stage_prologue(k, t, lst, true);
     if (ps != DEX_OK) return ps;
     return run_layers(ctx, lst, ls.front(), ls.back(), M, t, ctx->h_w + (size_t)r0 * ctx->d,
                       ctx->part_w + (size_t)r0 * ctx->n_part,
@@ -1424,10 +1424,33 @@ dex_status dex_step(dex_ctx *ctx, int32_t *committed_out, dex_step_info *info) {
     size_t depth = 0;
     for (int k = 0; k < N; ++k) {
       if (stage_lane[k] != lane) continue;
-      const dex_status ps = stage_prologue(k, tabs[k], st);
+      const dex_status ps = stage_prologue(k, tabs[k], st, false);
       if (ps != DEX_OK) return ps;
       ks.push_back(k);
       depth = std::max(depth, ctx->stage_layers[k].size());
+    }
+    // the stages' first RMSNorm inputs: one launch per run of at most
+    // MAX_SEGS stages (a lane's stages are consecutive among those with
+    // rows, so their rows are consecutive; stage 0, if present, comes first)
+    for (size_t i0 = 0; i0 < ks.size(); i0 += MAX_SEGS) {
+      const size_t c = std::min<size_t>(MAX_SEGS, ks.size() - i0);
+      const int ra = stage_r0[ks[i0]], rb = stage_r0[ks[i0 + c - 1] + 1];
+      PrepArgs p{};
+      p.M = rb - ra; p.d = ctx->d; p.n_part = ctx->n_part;
+      p.embed_rows = ks[i0] == 0 ? stage_r0[1] - stage_r0[0] : 0;
+      p.row_tok = dptr(t_tok) + ra; p.row_src = dptr(t_bnd) + ra;
+      p.embed = ctx->embed; p.bnd_h = ctx->bnd_h; p.bnd_part = ctx->bnd_part;
+      p.n_seg = (int)c;
+      for (size_t i = 0; i < c; ++i) {
+        const int k = ks[i0 + i];
+        p.seg_end[i] = stage_r0[k + 1] - ra;
+        p.seg_g[i] = (const float *)LW(ctx, ctx->stage_layers[k].front(), DEX_P_ATTN_NORM);
+      }
+      p.g = p.seg_g[0];
+      p.h = ctx->h_w + (size_t)ra * ctx->d; p.part = ctx->part_w + (size_t)ra * ctx->n_part;
+      p.xb = (char *)ctx->xb_w + (size_t)ra * ctx->d * ctx->es;
+      TimedLaunch tl(ctx, 7, 0.0);
+      HIPCHK(launch_prep(ctx->dtype, p, st));
     }
     // split records of every row of the round: [R][H][jmax][hd], then the
     // statistics

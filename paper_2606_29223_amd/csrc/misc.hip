@@ -28,13 +28,21 @@ template <typename T>
 __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(PrepArgs a) {
   constexpr int EPV = 16 / (int)sizeof(T);     // elements per 16-byte vector
   const int m = blockIdx.x;
+  const bool from_embed = m < a.embed_rows;
+  const float *gain = a.g;
+  if (a.n_seg > 0) {
+    int k = 0;
+#pragma unroll
+    for (int i = 0; i < MAX_SEGS - 1; ++i) k += (i < a.n_seg - 1 && m >= a.seg_end[i]) ? 1 : 0;
+    gain = a.seg_g[k];
+  }
   const int t = blockIdx.y * PREP_THREADS + threadIdx.x;
   if (t >= a.n_part) return;
   const int mo = (a.row_out != nullptr) ? a.row_out[m] : m;
   const int c0 = 16 * t;
   float v[16], g[16];
   float pin = 0.f;
-  if (a.from_embed) {
+  if (from_embed) {
     const uint4 *e = (const uint4 *)((const T *)a.embed + (size_t)a.row_tok[m] * a.d + c0);
     uint4 raw[16 / EPV];
 #pragma unroll
@@ -57,7 +65,7 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(PrepArgs a) {
     }
     pin = a.bnd_part[(size_t)a.row_src[m] * a.n_part + t];
   }
-  const float4 *gp = (const float4 *)(a.g + c0);
+  const float4 *gp = (const float4 *)(gain + c0);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float4 x = gp[q];
@@ -83,7 +91,7 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(PrepArgs a) {
       xb[q] = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
-  if (a.from_embed) {
+  if (from_embed) {
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < 16; ++j) s += v[j] * v[j];
@@ -95,6 +103,7 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(PrepArgs a) {
 hipError_t launch_prep(int dtype, const PrepArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.d % 16 != 0 || a.n_part * 16 != a.d) return hipErrorInvalidValue;
+  if (a.n_seg < 0 || a.n_seg > MAX_SEGS || (a.n_seg > 0 && a.seg_end[a.n_seg - 1] != a.M)) return hipErrorInvalidValue;
   const dim3 grid(a.M, (a.n_part + PREP_THREADS - 1) / PREP_THREADS);
   if (dtype == 1) hipLaunchKernelGGL(prep_kernel<bf16>, grid, dim3(PREP_THREADS), 0, s, a);
   else hipLaunchKernelGGL(prep_kernel<float>, grid, dim3(PREP_THREADS), 0, s, a);
