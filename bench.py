@@ -304,8 +304,14 @@ def main():
                                                             / PEAK_HBM_GBS, 4),
                                        "note": "single-layer launches of the class in the traced run; launches "
                                                "of concurrent stage lanes overlap and share HBM, which lengthens "
-                                               "some (the mean) but not the typical one (the median)",
+                                               "some (the mean) but not the typical one (the median); 'alone': "
+                                               "the launches during which no other kernel ran",
                                        "profile": os.path.relpath(args.kernel_stats_json, ROOT)}
+                if "avg_alone_us" in ent:
+                    roofline["rocprof"].update({
+                        "alone_launches": ent["launches_alone"],
+                        "alone_avg_launch_us": round(ent["avg_alone_us"], 2),
+                        "alone_frac": round(bytes_per / (ent["avg_alone_us"] * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)})
         except (OSError, ValueError, KeyError):
             pass
 

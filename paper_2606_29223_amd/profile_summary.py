@@ -139,18 +139,42 @@ def stats(args):
         # roofline next to its own timing
         cls_of = {"gemm_kernel<unsigned short, 1,": "qkv", "gemm_kernel<unsigned short, 3,": "gate_up",
                   "gemm_kernel<unsigned short, 4,": "lm_head", "gemm_kernel<unsigned short, 2,": "o_proj+down"}
-        per = {}
-        for t in trace:
+        # a launch ran alone when no other kernel of the run was active at
+        # any point of its span (launches of concurrent stage lanes share HBM)
+        span = sorted((int(t["Start_Timestamp"]), int(t["End_Timestamp"]), i) for i, t in enumerate(trace))
+        alone = [True] * len(trace)
+        far_end, far_i = -1, -1
+        for s0, e0, i in span:
+            if s0 < far_end:
+                alone[i] = False
+                alone[far_i] = False
+            if e0 > far_end:
+                far_end, far_i = e0, i
+        per, per_alone = {}, {}
+        for i, t in enumerate(trace):
             n = _short(t["Kernel_Name"])
             dur = (int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e3
             for k, c in cls_of.items():
                 if n.startswith(k):
                     per.setdefault(c, {}).setdefault(n, []).append(dur)
+                    if alone[i]:
+                        per_alone.setdefault(c, {}).setdefault(n, []).append(dur)
         classes = {}
         for c, insts in per.items():
             n, v = max(insts.items(), key=lambda kv: len(kv[1]))     # the most launched instantiation
             classes[c] = {"kernel": n, "launches": len(v), "avg_us": statistics.fmean(v),
                           "median_us": statistics.median(v)}
+            va = per_alone.get(c, {}).get(n, [])
+            if va:
+                classes[c].update({"launches_alone": len(va), "avg_alone_us": statistics.fmean(va),
+                                   "median_alone_us": statistics.median(va)})
+        lines += ["", "decode GEMM classes, most launched instantiation: mean over all launches, and over the",
+                  "launches that ran alone (no other kernel active during their span)"]
+        for c in sorted(classes):
+            e = classes[c]
+            lines.append(f"  {c:12s} {e['kernel']:42s} all {e['launches']:6d} x {e['avg_us']:7.2f} us"
+                         + (f"   alone {e['launches_alone']:6d} x {e['avg_alone_us']:7.2f} us" if "avg_alone_us" in e
+                            else ""))
         json.dump({"source": csrc_source_hash(), "config": args.config, "command": args.command,
                    "classes": classes}, open(args.out_json, "w"), indent=1)
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
